@@ -1,0 +1,317 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged-KV attention hot path on one MI355X.
+
+Headline (one JSON line on stdout): decode of the Llama-3-8B-shaped layer
+(256 sequences, lengths U[512, 4096], bf16) as algorithmic KV-read GB/s. A
+step is one kvattn_decode call over the whole batch, inputs resident in HBM.
+The same line carries the chunked-prefill figures (the last 8192-token chunk
+of a 32768-token prompt and the whole 32768-token prompt, TFLOP/s), the
+elastic-pool toggle latencies, the roofline of the dominant kernel from
+per-kernel HIP events, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import resource
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="all",
+                    choices=["all", "decode", "prefill", "mixed", "toggle"],
+                    help="'all' = headline decode plus the prefill, mixed-step and toggle legs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+class Timer:
+    """HIP events on the current stream around a region."""
+
+    def __init__(self):
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def __enter__(self):
+        torch.cuda.synchronize()
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        torch.cuda.synchronize()
+        self.ms = self.a.elapsed_time(self.b)
+        return False
+
+
+def timed(fn, steps, warmup, K, kernel):
+    """Run fn warmup + steps times; returns (ms per step, mean ms of `kernel`
+    launches from per-kernel events, all per-kernel means)."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    with K.KernelTrace(4 * steps) as tr:
+        with Timer() as t:
+            for _ in range(steps):
+                fn()
+    per = {}
+    for name, ms in tr.durations():
+        per.setdefault(name, []).append(ms)
+    means = {k: statistics.fmean(v) for k, v in per.items()}
+    return t.ms / steps, means.get(kernel), means
+
+
+def roofline_hbm(bytes_per_launch, kernel_ms):
+    ach = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+
+
+def roofline_mfma(flops_per_launch, kernel_ms):
+    ach = flops_per_launch / (kernel_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+
+
+def decode_leg(args, K, work, wl):
+    from workloads import config_spec, make_batch
+    spec = config_spec(2)
+    log("decode: generating", spec.name)
+    b = make_batch(spec)
+    q = b.q.cuda()
+    kv = b.kv_layer.cuda()
+    bt = torch.from_numpy(b.block_table).cuda()
+    sl = torch.from_numpy(b.seq_lens).cuda()
+    out = torch.empty_like(q)
+    ws = K.workspace(K.decode_workspace_bytes(b.num_seqs, 32, 128, b.max_seq_len))
+
+    def step():
+        K.decode(q, kv, b.num_blocks, bt, sl, num_kv_heads=8, max_seq_len=b.max_seq_len,
+                 scale=b.scale, out=out, ws=ws)
+
+    ms, kern_ms, means = timed(step, args.steps, args.warmup, K, "decode_split")
+    nbytes = work.decode_bytes(b.seq_lens, 32, 8, 128, 2)
+    kvb = work.decode_kv_bytes(b.seq_lens, 8, 128, 2)
+    log(f"decode: {ms * 1e3:.1f} us/step, kernels {means}")
+    res = {
+        "workload": spec.name, "ms_per_step": ms,
+        "gbs": nbytes / (ms * 1e-3) / 1e9,
+        "kv_gbs": kvb / (ms * 1e-3) / 1e9,
+        "bytes_per_step": nbytes, "kernel_ms": means,
+        "roofline": roofline_hbm(nbytes, kern_ms),
+        "num_seqs": b.num_seqs, "sum_seq_len": int(b.seq_lens.sum()),
+    }
+    return res, b
+
+
+def prefill_leg(args, K, work):
+    from workloads import config_spec, make_batch
+    spec = config_spec(4)
+    log("prefill: generating", spec.name)
+    b = make_batch(spec)
+    q = b.q.cuda()
+    kv = b.kv_layer.cuda()
+    bt = torch.from_numpy(b.block_table).cuda()
+    res = {}
+    out = torch.empty_like(q)
+    ws = K.workspace(K.prefill_workspace_bytes(1, 32768, 32, 128))
+    # (a) the last 8192-token chunk over 24576 cached tokens; (b) the whole prompt
+    for name, n, L in (("chunk8192_ctx24576", 8192, 32768), ("whole32768", 32768, 32768)):
+        qq = q[L - n:L]
+        oo = out[:n]
+        sl = torch.tensor([L], dtype=torch.int32, device="cuda")
+        cu = torch.tensor([0, n], dtype=torch.int32, device="cuda")
+
+        def step():
+            K.prefill_chunk(qq, kv, b.num_blocks, bt, sl, cu, num_kv_heads=8, max_seq_len=L,
+                            max_num_batched_tokens=n, scale=b.scale, out=oo, ws=ws)
+
+        steps = max(3, args.steps // 5)
+        ms, kern_ms, means = timed(step, steps, max(1, args.warmup // 2), K, "prefill")
+        flops = work.prefill_flops([L], [n], 32, 128)
+        log(f"prefill {name}: {ms:.3f} ms/call, {flops / ms / 1e9:.1f} TFLOP/s, kernels {means}")
+        res[name] = {"ms_per_call": ms, "tflops": flops / (ms * 1e-3) / 1e12,
+                     "flops_per_call": flops, "kernel_ms": means,
+                     "roofline": roofline_mfma(flops, kern_ms)}
+    return res, b
+
+
+def mixed_leg(args, K, work):
+    """The mixed step: one prefill call (8192 new rows of a 32768-token prompt)
+    and one decode call (128 sequences), back to back on one stream."""
+    from workloads import config_spec, make_batch
+    spec = config_spec(3)
+    log("mixed: generating", spec.name)
+    b = make_batch(spec)
+    q = b.q.cuda()
+    kv = b.kv_layer.cuda()
+    bt = torch.from_numpy(b.block_table).cuda()
+    sl = torch.from_numpy(b.seq_lens).cuda()
+    qp, qd = q[:8192], q[8192:]
+    op, od = torch.empty_like(qp), torch.empty_like(qd)
+    slp = sl[:1]
+    cup = torch.tensor([0, 8192], dtype=torch.int32, device="cuda")
+    wsp = K.workspace(K.prefill_workspace_bytes(1, 8192, 32, 128))
+    wsd = K.workspace(K.decode_workspace_bytes(128, 32, 128, b.max_seq_len))
+
+    def step():
+        K.prefill_chunk(qp, kv, b.num_blocks, bt[:1], slp, cup, num_kv_heads=8,
+                        max_seq_len=b.max_seq_len, max_num_batched_tokens=8192 + 128,
+                        scale=b.scale, out=op, ws=wsp)
+        K.decode(qd, kv, b.num_blocks, bt[1:], sl[1:], num_kv_heads=8,
+                 max_seq_len=b.max_seq_len, scale=b.scale, out=od, ws=wsd)
+
+    steps = max(3, args.steps // 5)
+    ms, _, means = timed(step, steps, max(1, args.warmup // 2), K, "prefill")
+    flops = work.prefill_flops(b.seq_lens[:1], b.q_lens[:1], 32, 128)
+    dbytes = work.decode_bytes(b.seq_lens[1:], 32, 8, 128, 2)
+    log(f"mixed: {ms:.3f} ms/step, kernels {means}")
+    return {"workload": spec.name, "ms_per_step": ms, "kernel_ms": means,
+            "prefill_tflops": flops / (means["prefill"] * 1e-3) / 1e12,
+            "decode_gbs": dbytes / (means["decode_split"] * 1e-3) / 1e9}
+
+
+def toggle_leg(K):
+    """Commit / decommit of a 3 GiB elastic reserve spread over 32 layers."""
+    from workloads.configs import ELASTIC
+    gran = max(K.ElasticPool.granularity(), 2 << 20)
+    el = ELASTIC.elastic_bytes_per_layer
+    assert el % gran == 0
+    base = 64 * gran
+    pool = K.ElasticPool(ELASTIC.num_layers, base, el)
+    commit, decommit, bd_c, bd_d = [], [], [], []
+    try:
+        for i in range(22):
+            c = pool.commit()
+            bc = pool.last_breakdown()
+            d = pool.decommit()
+            bdd = pool.last_breakdown()
+            if i >= 2:
+                commit.append(c)
+                decommit.append(d)
+                bd_c.append(bc)
+                bd_d.append(bdd)
+    finally:
+        pool.close()
+    med = statistics.median
+    res = {"reserve_bytes": el * ELASTIC.num_layers, "layers": ELASTIC.num_layers,
+           "granularity": gran, "cycles": len(commit),
+           "commit_ms_median": med(commit), "decommit_ms_median": med(decommit),
+           "commit_breakdown_ms": {k: med([x[k] for x in bd_c])
+                                   for k in ("create_ms", "map_ms", "access_ms")},
+           "decommit_breakdown_ms": {k: med([x[k] for x in bd_d])
+                                     for k in ("sync_ms", "unmap_ms")}}
+    log(f"toggle: commit {res['commit_ms_median']:.2f} ms, decommit "
+        f"{res['decommit_ms_median']:.2f} ms")
+    return res
+
+
+def cpu_baseline(b, work, seconds):
+    """The fp64 oracle on the first sequences of the decode batch, as many as
+    fit in about `seconds` of wall time; reported in the headline's unit."""
+    import oracle
+    seqs, t0 = [], time.perf_counter()
+    r0 = resource.getrusage(resource.RUSAGE_SELF)
+    for s in range(b.num_seqs):
+        oracle.paged_decode(b.q_raw(), b.kv_raw(), b.block_table, b.seq_lens, dtype=b.dtype,
+                            num_q_heads=b.num_q_heads, num_kv_heads=b.num_kv_heads,
+                            head_dim=b.head_dim, block_size=b.block_size, scale=b.scale,
+                            seqs=[s])
+        seqs.append(s)
+        if time.perf_counter() - t0 > seconds:
+            break
+    wall = time.perf_counter() - t0
+    r1 = resource.getrusage(resource.RUSAGE_SELF)
+    cpu = (r1.ru_utime - r0.ru_utime) + (r1.ru_stime - r0.ru_stime)
+    lens = b.seq_lens[seqs]
+    nbytes = work.decode_bytes(lens, b.num_q_heads, b.num_kv_heads, b.head_dim, b.esz)
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(nbytes / wall / 1e9, 4), "unit": "GB/s",
+            "cores": round(cpu / wall, 2), "kind": "oracle",
+            "sample": f"fp64 oracle decode of the first {len(seqs)} of {b.num_seqs} sequences "
+                      f"({int(lens.sum())} context tokens, {nbytes} algorithmic bytes) in "
+                      f"{wall:.1f} s wall, {cpu:.1f} s CPU",
+            "cpu_model": model, "threads_available": len(os.sched_getaffinity(0))}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the hot path has no multi-GPU form here "
+              "(sharding is by KV head or by sequence with no exchange; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_2608_23658_amd.kvattn as K
+    from paper_2608_23658_amd import work
+    K.lib()
+
+    line = {"metric": "decode attn KV-read GB/s (% HBM peak); chunked-prefill attn TFLOP/s "
+                      "(% MFMA)",
+            "value": None, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": None}
+    dec_batch = None
+    if args.workload in ("all", "decode"):
+        dec, dec_batch = decode_leg(args, K, work, None)
+        line["value"] = round(dec["gbs"], 1)
+        line["ms_per_step"] = round(dec["ms_per_step"], 5)
+        line["config"] = {"workload": dec["workload"], "num_seqs": dec["num_seqs"],
+                          "seq_len": "U[512,4096]", "sum_seq_len": dec["sum_seq_len"],
+                          "num_q_heads": 32, "num_kv_heads": 8, "head_dim": 128,
+                          "block_size": 16, "parallelism": "none (1 GPU)"}
+        line["roofline"] = dec["roofline"]
+        line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms")}
+    if args.workload in ("all", "prefill"):
+        pre, _ = prefill_leg(args, K, work)
+        line["prefill"] = pre
+        if line["value"] is None:
+            p = pre["chunk8192_ctx24576"]
+            line.update(value=round(p["tflops"], 2), unit="TFLOP/s",
+                        ms_per_step=round(p["ms_per_call"], 5), roofline=p["roofline"],
+                        config={"workload": "prefill_chunk8192_ctx24576_bf16"})
+    if args.workload in ("all", "mixed"):
+        line["mixed_step"] = mixed_leg(args, K, work)
+    if args.workload in ("all", "toggle"):
+        line["elastic_toggle"] = toggle_leg(K)
+    if dec_batch is not None and not args.no_cpu_baseline:
+        log("cpu baseline: oracle sample")
+        line["cpu_baseline"] = cpu_baseline(dec_batch, work, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

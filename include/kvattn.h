@@ -1,0 +1,207 @@
+/*
+ * kvattn: attention over a block-indexed paged KV cache on one MI355X
+ * (gfx950), and the elastic per-layer VMM pool the cache lives in.
+ *
+ * C ABI: plain pointers and sizes only. Every entry point returns a
+ * kv_status; a failure leaves a message readable via kv_last_error()
+ * (thread-local). Nothing crosses the boundary as an exception or abort.
+ *
+ * ---------------------------------------------------------------------------
+ * Paged KV layout of one layer (the paper, Section 3 "The contiguity
+ * constraint": one contiguous tensor per layer, indexed by block id through a
+ * single base pointer). Block-major, so that the top block ids are the top of
+ * the address range, which is where the elastic sub-range maps (Section 3,
+ * "Two handles, one virtual range"):
+ *
+ *   layer[num_blocks][2 (K=0, V=1)][num_kv_heads][block_size * head_dim]
+ *
+ * One (block, K/V, kv head) tile of block_size * head_dim elements:
+ *   K tile, chunk-major: token slot r, dim j at
+ *       ((j / VEC) * block_size + r) * VEC + (j % VEC),  VEC = 16 / element size
+ *   V tile, dim-major (transposed): token slot r, dim j at  j * block_size + r
+ * Element type is the call's kv_dtype (fp32 or bf16). Token t of sequence s
+ * is slot t % block_size of block block_table[s * max_blocks_per_seq + t /
+ * block_size].
+ *
+ * Attention computed (Section 5, "Why the penalty is small": a chunk attends
+ * to all prior context, decode is one token per sequence): for sequence s
+ * with L_s context tokens of which the last n_s are new, new row i (absolute
+ * position p = L_s - n_s + i), query head h, kv head g = h / (Hq / Hkv):
+ *   out = sum_{t <= p} softmax_t(scale * q . K_s[t]) V_s[t]
+ * Softmax accumulates in fp32; bf16 outputs are rounded to nearest even.
+ * ---------------------------------------------------------------------------
+ */
+#ifndef KVATTN_H
+#define KVATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KV_OK = 0,
+  KV_ERR_INVALID = -1,      /* bad argument: shape, alignment, size, null pointer */
+  KV_ERR_UNSUPPORTED = -2,  /* valid but not built: head_dim, group size, dtype */
+  KV_ERR_HIP = -3,          /* a HIP runtime call failed */
+  KV_ERR_OOM = -4,          /* physical memory could not be created */
+  KV_ERR_STATE = -5         /* call not allowed in the pool's current state */
+} kv_status;
+
+typedef enum { KV_F32 = 0, KV_BF16 = 1 } kv_dtype;
+
+/* Message of the calling thread's last failure ("" if none). Owned by the
+ * library; valid until the thread's next call into it. */
+const char* kv_last_error(void);
+
+/* ABI version, bumped on any signature or layout change. */
+int kvattn_abi_version(void);
+
+/* ------------------------------------------------------------------------- */
+/* Decode: one new query token per sequence (Section 5). Split-K over the
+ * context: each (sequence, kv head, split of the context) is one workgroup,
+ * whose partial softmax state is merged by a second kernel.
+ *
+ * Workspace: device memory of at least kvattn_decode_workspace_bytes(...)
+ * bytes, owned by the caller, 256-byte aligned, no initial contents needed,
+ * must not be used by another call in flight. Returns 0 if the sizes are
+ * invalid. */
+size_t kvattn_decode_workspace_bytes(int num_seqs, int num_q_heads, int head_dim,
+                                     int max_seq_len);
+
+/* Context tokens per split used by kvattn_decode for a batch whose longest
+ * sequence is max_seq_len (a multiple of 64; depends on nothing else, so a
+ * sequence's arithmetic depends only on its own length). */
+int kvattn_decode_split_tokens(int max_seq_len);
+
+/*
+ * q            device, [num_seqs][num_q_heads][head_dim] of dtype, 16-B aligned
+ * kv_layer     device, base of one layer in the layout above, 16-B aligned
+ * num_blocks   blocks in the layer; block ids outside [0, num_blocks) are
+ *              skipped (they contribute nothing) rather than read
+ * block_table  device int32 [num_seqs][max_blocks_per_seq]; entries past
+ *              ceil(seq_len / block_size) are never read (pad with -1)
+ * seq_lens     device int32 [num_seqs], 0 <= seq_len <= max_seq_len and
+ *              <= max_blocks_per_seq * block_size; the query token is the
+ *              last of its sequence. A sequence of length 0 gets zeros.
+ * out          device, [num_seqs][num_q_heads][head_dim] of dtype, 16-B aligned
+ * scale        softmax scale (1/sqrt(head_dim) for standard attention)
+ * stream       hipStream_t to enqueue on (NULL: the null stream)
+ *
+ * Supported: block_size 16; num_q_heads / num_kv_heads in {1, 2, 4, 8}; bf16
+ * with head_dim 64 or 128, fp32 with head_dim 64. Asynchronous: returns after enqueueing. The
+ * library allocates nothing.
+ */
+int kvattn_decode(const void* q, const void* kv_layer, int num_blocks,
+                  const int32_t* block_table, const int32_t* seq_lens, void* out,
+                  int num_seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                  int block_size, int max_blocks_per_seq, int max_seq_len, float scale,
+                  kv_dtype dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Kernel tracing. While a trace buffer is installed on the calling thread,
+ * every kernel the library launches from that thread is bracketed by
+ * hipEventRecord of the next two events of the buffer (hipEvent_t handles
+ * owned by the caller) on the launch stream, so per-kernel durations can be
+ * read with hipEventElapsedTime. Launches beyond the buffer are not traced.
+ * kvattn_trace_end uninstalls the buffer and reports the events used. */
+int kvattn_trace_begin(void* const* events, int capacity);
+int kvattn_trace_end(int* events_used);
+/* Name of the kernel traced by events 2i and 2i+1 of the last trace ("" if none). */
+const char* kvattn_trace_kernel_name(int i);
+
+/* ------------------------------------------------------------------------- */
+/* Chunked prefill (Section 5 and Section 1: max_num_batched_tokens bounds the
+ * new tokens of one step; a chunk attends causally to itself and to all of
+ * its sequence's earlier tokens, which are already in the cache).
+ *
+ * q             device, [total_q_tokens][num_q_heads][head_dim] bf16, 16-B aligned
+ * kv_layer      as for decode; the chunk's own K/V must already be written
+ * block_table   as for decode
+ * seq_lens      device int32 [num_seqs]: context length INCLUDING the chunk
+ * cu_seqlens_q  device int32 [num_seqs + 1], nondecreasing from 0: the chunk of
+ *               sequence s is rows [cu[s], cu[s+1]) of q and out, with
+ *               cu[s+1] - cu[s] <= seq_lens[s]; cu[num_seqs] == total_q_tokens
+ * out           device, [total_q_tokens][num_q_heads][head_dim] bf16
+ * max_num_batched_tokens  the step's token budget: total_q_tokens must not
+ *               exceed it (KV_ERR_INVALID otherwise); it sizes no buffer and
+ *               never changes the arithmetic
+ * workspace     device scratch of kvattn_prefill_workspace_bytes(...) bytes
+ *
+ * Causal alignment is bottom-right: row i of sequence s sees keys
+ * 0 .. seq_lens[s] - n_s + i. Supported: bf16, block_size 16, head_dim 128,
+ * num_q_heads / num_kv_heads in {1, 2, 4}; KV_F32 returns KV_ERR_UNSUPPORTED.
+ * Asynchronous; allocates nothing.
+ */
+size_t kvattn_prefill_workspace_bytes(int num_seqs, int total_q_tokens, int num_q_heads,
+                                      int head_dim);
+
+int kvattn_prefill_chunk(const void* q, const void* kv_layer, int num_blocks,
+                         const int32_t* block_table, const int32_t* seq_lens,
+                         const int32_t* cu_seqlens_q, void* out, int num_seqs,
+                         int total_q_tokens, int max_num_batched_tokens, int num_q_heads,
+                         int num_kv_heads, int head_dim, int block_size,
+                         int max_blocks_per_seq, int max_seq_len, float scale,
+                         kv_dtype dtype, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Elastic per-layer KV pool (Section 3, "Two handles, one virtual range").
+ * Each layer owns one reserved virtual range of base + elastic bytes plus one
+ * unmapped guard granule. A base physical handle backs [0, base) for the
+ * pool's life; an elastic handle backs [base, base + elastic) only while
+ * committed. Layer pointers never move, so kernels and captured graphs keep
+ * working across toggles. Sizes must be multiples of kvpool_granularity(). */
+typedef struct kvpool kvpool;
+
+/* Minimum VMM granularity of the device, in bytes. */
+int kvpool_granularity(int device, size_t* bytes);
+
+/* Reserve and map every layer's base sub-range; the elastic sub-ranges start
+ * decommitted. On failure nothing stays allocated and *out is NULL.
+ * KV_ERR_OOM if the base handles cannot be created. */
+int kvpool_create(int device, int num_layers, size_t base_bytes_per_layer,
+                  size_t elastic_bytes_per_layer, kvpool** out);
+
+/* Base address of a layer's range; stable for the pool's lifetime. */
+int kvpool_layer_ptr(const kvpool* pool, int layer, void** ptr);
+
+/* 1 if the elastic sub-ranges are mapped, 0 if not, <0 on a bad pool. */
+int kvpool_is_committed(const kvpool* pool);
+
+/* Commit: for every layer create an elastic physical handle, map it at the
+ * top of the layer's range and grant the device read/write access. Synchronous:
+ * the memory is usable from any stream on return. Committing a committed pool
+ * is a successful no-op. If any layer's handle cannot be created, every handle
+ * made so far is released, the pool stays decommitted with its base contents
+ * intact, and KV_ERR_OOM is returned. Contents of freshly committed memory are
+ * undefined. elapsed_ms (nullable) receives the host wall time of the call. */
+int kvpool_commit_elastic(kvpool* pool, double* elapsed_ms);
+
+/* Decommit: wait for all work on the device to finish, then unmap and release
+ * every layer's elastic handle, returning the memory to the device (Section 3,
+ * "Controller": drain, sync, unmap). The caller must first stop handing out
+ * elastic block ids. Decommitting a decommitted pool is a successful no-op.
+ * elapsed_ms (nullable) receives the host wall time of the call. */
+int kvpool_decommit_elastic(kvpool* pool, double* elapsed_ms);
+
+/* Sizes as created. */
+int kvpool_sizes(const kvpool* pool, int* num_layers, size_t* base_bytes_per_layer,
+                 size_t* elastic_bytes_per_layer);
+
+/* Host wall-time breakdown of the last commit (create, map, set access) and
+ * of the last decommit (device sync, unmap + release), in milliseconds.
+ * Any output pointer may be NULL. */
+int kvpool_last_toggle_breakdown(const kvpool* pool, double* create_ms, double* map_ms,
+                                 double* access_ms, double* sync_ms, double* unmap_ms);
+
+/* Decommit if needed, unmap the base handles, free the ranges. NULL is a no-op. */
+void kvpool_destroy(kvpool* pool);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVATTN_H */

@@ -1,0 +1,288 @@
+// C-ABI entry points for paged-KV attention: argument checks, workspace
+// sizing and kernel launches. No allocation happens here.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "abi_internal.hpp"
+#include "kvattn.h"
+#include "launch.hpp"
+
+namespace kvattn {
+
+namespace {
+thread_local std::string g_error;
+}
+
+int set_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+void clear_error() { g_error.clear(); }
+
+namespace {
+struct Trace {
+  void* const* events = nullptr;
+  int capacity = 0;
+  int used = 0;
+  std::vector<std::string> names;
+};
+thread_local Trace g_trace;
+thread_local std::vector<std::string> g_last_names;
+}  // namespace
+
+void trace_before(hipStream_t stream, const char* kernel) {
+  Trace& t = g_trace;
+  if (!t.events || t.used + 2 > t.capacity) return;
+  (void)hipEventRecord(static_cast<hipEvent_t>(t.events[t.used]), stream);
+  t.names.emplace_back(kernel);
+}
+
+void trace_after(hipStream_t stream) {
+  Trace& t = g_trace;
+  if (!t.events || t.used + 2 > t.capacity) return;
+  (void)hipEventRecord(static_cast<hipEvent_t>(t.events[t.used + 1]), stream);
+  t.used += 2;
+}
+
+}  // namespace kvattn
+
+using kvattn::clear_error;
+using kvattn::set_error;
+
+namespace {
+
+constexpr int kAbiVersion = 1;
+constexpr int kDecodeSplitTokens = 512;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+struct DecodeWs {
+  size_t ml_offset;
+  size_t total;
+};
+
+bool decode_ws(int num_seqs, int num_q_heads, int head_dim, int max_seq_len, DecodeWs* w) {
+  if (num_seqs < 0 || num_q_heads <= 0 || head_dim <= 0 || max_seq_len < 0) return false;
+  const int split = kvattn_decode_split_tokens(max_seq_len);
+  const size_t splits = max_seq_len > 0 ? (size_t)(max_seq_len + split - 1) / split : 1;
+  const size_t n = (size_t)num_seqs * num_q_heads * splits;
+  w->ml_offset = align256(n * head_dim * sizeof(float));
+  w->total = w->ml_offset + align256(n * 2 * sizeof(float));
+  if (w->total == 0) w->total = 256;
+  return true;
+}
+
+bool group_ok(int hq, int hkv, int max_group) {
+  if (hq <= 0 || hkv <= 0 || hq % hkv) return false;
+  const int g = hq / hkv;
+  return g == 1 || g == 2 || g == 4 || (g == 8 && max_group >= 8);
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return KV_OK;
+  (void)hipGetLastError();   // the runtime keeps the error sticky: clear it for the caller
+  return set_error(KV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" const char* kv_last_error(void) { return kvattn::g_error.c_str(); }
+
+extern "C" int kvattn_abi_version(void) { return kAbiVersion; }
+
+extern "C" int kvattn_trace_begin(void* const* events, int capacity) {
+  clear_error();
+  if (!events || capacity < 2)
+    return set_error(KV_ERR_INVALID, "kvattn_trace_begin: need at least 2 events");
+  kvattn::g_trace = kvattn::Trace{};
+  kvattn::g_trace.events = events;
+  kvattn::g_trace.capacity = capacity;
+  return KV_OK;
+}
+
+extern "C" int kvattn_trace_end(int* events_used) {
+  clear_error();
+  if (events_used) *events_used = kvattn::g_trace.used;
+  kvattn::g_last_names = kvattn::g_trace.names;
+  kvattn::g_trace = kvattn::Trace{};
+  return KV_OK;
+}
+
+extern "C" const char* kvattn_trace_kernel_name(int i) {
+  if (i < 0 || i >= (int)kvattn::g_last_names.size()) return "";
+  return kvattn::g_last_names[i].c_str();
+}
+
+extern "C" int kvattn_decode_split_tokens(int max_seq_len) {
+  (void)max_seq_len;
+  return kDecodeSplitTokens;
+}
+
+extern "C" size_t kvattn_decode_workspace_bytes(int num_seqs, int num_q_heads, int head_dim,
+                                                int max_seq_len) {
+  DecodeWs w;
+  return decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w) ? w.total : 0;
+}
+
+extern "C" int kvattn_decode(const void* q, const void* kv_layer, int num_blocks,
+                             const int32_t* block_table, const int32_t* seq_lens, void* out,
+                             int num_seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                             int block_size, int max_blocks_per_seq, int max_seq_len,
+                             float scale, kv_dtype dtype, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (num_seqs < 0) return set_error(KV_ERR_INVALID, "kvattn_decode: num_seqs %d < 0", num_seqs);
+  if (dtype != KV_F32 && dtype != KV_BF16)
+    return set_error(KV_ERR_INVALID, "kvattn_decode: unknown dtype %d", (int)dtype);
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
+    return set_error(KV_ERR_INVALID, "kvattn_decode: %d query heads over %d kv heads",
+                     num_q_heads, num_kv_heads);
+  if (!group_ok(num_q_heads, num_kv_heads, 8))
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: group size %d not built",
+                     num_q_heads / num_kv_heads);
+  if (head_dim != 64 && !(head_dim == 128 && dtype == KV_BF16))
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: head_dim %d not built for %s",
+                     head_dim, dtype == KV_BF16 ? "bf16" : "fp32");
+  if (block_size != 16)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: block_size %d not built", block_size);
+  if (max_blocks_per_seq <= 0 || max_seq_len < 0 ||
+      (long long)max_seq_len > (long long)max_blocks_per_seq * block_size)
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_decode: max_seq_len %d does not fit %d blocks of %d tokens",
+                     max_seq_len, max_blocks_per_seq, block_size);
+  if (num_blocks <= 0) return set_error(KV_ERR_INVALID, "kvattn_decode: num_blocks %d", num_blocks);
+  if (!std::isfinite(scale)) return set_error(KV_ERR_INVALID, "kvattn_decode: scale not finite");
+  if (num_kv_heads > 65535 || num_seqs > 65535)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: grid too large");
+  if (num_seqs == 0) return KV_OK;
+  if (!q || !kv_layer || !block_table || !seq_lens || !out || !workspace)
+    return set_error(KV_ERR_INVALID, "kvattn_decode: null pointer argument");
+  if (!aligned16(q) || !aligned16(kv_layer) || !aligned16(out) || !aligned16(workspace))
+    return set_error(KV_ERR_INVALID, "kvattn_decode: q, kv_layer, out and workspace must be "
+                                     "16-byte aligned");
+  DecodeWs w;
+  decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w);
+  if (workspace_bytes < w.total)
+    return set_error(KV_ERR_INVALID, "kvattn_decode: workspace %zu bytes < %zu needed",
+                     workspace_bytes, w.total);
+
+  kvattn::DecodeArgs a;
+  a.q = q;
+  a.kv = kv_layer;
+  a.num_blocks = num_blocks;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.out = out;
+  a.num_seqs = num_seqs;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.max_blocks = max_blocks_per_seq;
+  a.max_seq_len = max_seq_len;
+  a.split_tokens = kvattn_decode_split_tokens(max_seq_len);
+  a.scale = scale;
+  a.bf16 = dtype == KV_BF16;
+  a.workspace = workspace;
+  a.ws_ml_offset = w.ml_offset;
+  a.stream = static_cast<hipStream_t>(stream);
+  return hip_status(kvattn::launch_decode(a), "kvattn_decode launch");
+}
+
+extern "C" size_t kvattn_prefill_workspace_bytes(int num_seqs, int total_q_tokens,
+                                                 int num_q_heads, int head_dim) {
+  if (num_seqs < 0 || total_q_tokens < 0 || num_q_heads <= 0 || head_dim <= 0) return 0;
+  // Work-tile list: one int2 per tile of kPrefillRows query rows of a sequence.
+  const size_t tiles = (size_t)total_q_tokens / kvattn::kPrefillRows + num_seqs + 1;
+  return align256(tiles * 2 * sizeof(int32_t) + 16);
+}
+
+extern "C" int kvattn_prefill_chunk(const void* q, const void* kv_layer, int num_blocks,
+                                    const int32_t* block_table, const int32_t* seq_lens,
+                                    const int32_t* cu_seqlens_q, void* out, int num_seqs,
+                                    int total_q_tokens, int max_num_batched_tokens,
+                                    int num_q_heads, int num_kv_heads, int head_dim,
+                                    int block_size, int max_blocks_per_seq, int max_seq_len,
+                                    float scale, kv_dtype dtype, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (dtype == KV_F32)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: fp32 prefill is not built");
+  if (dtype != KV_BF16)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: unknown dtype %d", (int)dtype);
+  if (num_seqs < 0 || total_q_tokens < 0)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: negative sizes");
+  if (total_q_tokens > max_num_batched_tokens)
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_prefill_chunk: %d new tokens exceed max_num_batched_tokens %d",
+                     total_q_tokens, max_num_batched_tokens);
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: %d query heads over %d kv heads",
+                     num_q_heads, num_kv_heads);
+  if (!group_ok(num_q_heads, num_kv_heads, 4))
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: group size %d not built",
+                     num_q_heads / num_kv_heads);
+  if (head_dim != 128)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: head_dim %d not built",
+                     head_dim);
+  if (block_size != 16)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: block_size %d not built",
+                     block_size);
+  if (max_blocks_per_seq <= 0 || max_seq_len < 0 ||
+      (long long)max_seq_len > (long long)max_blocks_per_seq * block_size)
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_prefill_chunk: max_seq_len %d does not fit %d blocks of %d tokens",
+                     max_seq_len, max_blocks_per_seq, block_size);
+  if (num_blocks <= 0)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: num_blocks %d", num_blocks);
+  if (!std::isfinite(scale))
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: scale not finite");
+  if (num_kv_heads > 65535) return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: grid");
+  if (num_seqs == 0 || total_q_tokens == 0) return KV_OK;
+  if (!q || !kv_layer || !block_table || !seq_lens || !cu_seqlens_q || !out || !workspace)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: null pointer argument");
+  if (!aligned16(q) || !aligned16(kv_layer) || !aligned16(out) || !aligned16(workspace))
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: q, kv_layer, out and workspace "
+                                     "must be 16-byte aligned");
+  const size_t need = kvattn_prefill_workspace_bytes(num_seqs, total_q_tokens, num_q_heads,
+                                                     head_dim);
+  if (workspace_bytes < need)
+    return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: workspace %zu bytes < %zu needed",
+                     workspace_bytes, need);
+  kvattn::PrefillArgs a;
+  a.q = q;
+  a.kv = kv_layer;
+  a.num_blocks = num_blocks;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.cu_seqlens_q = cu_seqlens_q;
+  a.out = out;
+  a.num_seqs = num_seqs;
+  a.total_q_tokens = total_q_tokens;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.max_blocks = max_blocks_per_seq;
+  a.max_seq_len = max_seq_len;
+  a.scale = scale;
+  a.workspace = workspace;
+  a.workspace_bytes = workspace_bytes;
+  a.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = kvattn::launch_prefill(a);
+  if (e == hipErrorNotSupported)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: kernel not built");
+  return hip_status(e, "kvattn_prefill_chunk launch");
+}

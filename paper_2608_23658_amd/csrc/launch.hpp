@@ -1,0 +1,52 @@
+// Host-side launch descriptors shared by the C ABI and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvattn {
+
+struct DecodeArgs {
+  const void* q;
+  const void* kv;
+  int num_blocks;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  void* out;
+  int num_seqs, num_q_heads, num_kv_heads, head_dim;
+  int max_blocks, max_seq_len, split_tokens;
+  float scale;
+  bool bf16;
+  void* workspace;
+  size_t ws_ml_offset;   // byte offset of the (m, l) partials in the workspace
+  hipStream_t stream;
+};
+
+struct PrefillArgs {
+  const void* q;
+  const void* kv;
+  int num_blocks;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const int32_t* cu_seqlens_q;
+  void* out;
+  int num_seqs, total_q_tokens, num_q_heads, num_kv_heads, head_dim;
+  int max_blocks, max_seq_len;
+  float scale;
+  void* workspace;
+  size_t workspace_bytes;
+  hipStream_t stream;
+};
+
+// Tracing hooks around each kernel launch (no-ops unless a trace is installed).
+void trace_before(hipStream_t stream, const char* kernel);
+void trace_after(hipStream_t stream);
+
+hipError_t launch_decode(const DecodeArgs& a);
+hipError_t launch_prefill(const PrefillArgs& a);
+
+// Query rows per prefill work tile (per query head).
+constexpr int kPrefillRows = 64;
+
+}  // namespace kvattn

@@ -1,0 +1,313 @@
+"""Thin Python binding of ``libkvattn.so`` (argument marshalling only).
+
+Every computation runs in the HIP library; this module passes device
+pointers, sizes and the current HIP stream through ``ctypes``. PyTorch is
+used for device memory (outputs, workspaces) and streams. If the library has
+not been built the functions raise: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkvattn.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "kvattn.h")
+
+KV_OK, KV_ERR_INVALID, KV_ERR_UNSUPPORTED, KV_ERR_HIP, KV_ERR_OOM, KV_ERR_STATE = 0, -1, -2, -3, -4, -5
+KV_F32, KV_BF16 = 0, 1
+_STATUS = {0: "KV_OK", -1: "KV_ERR_INVALID", -2: "KV_ERR_UNSUPPORTED", -3: "KV_ERR_HIP",
+           -4: "KV_ERR_OOM", -5: "KV_ERR_STATE"}
+
+_lib = None
+
+
+class KvAttnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _c(fn, restype, *argtypes):
+    fn.restype = restype
+    fn.argtypes = list(argtypes)
+    return fn
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2608_23658_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz, f32, dp = (ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_float,
+                            ctypes.POINTER(ctypes.c_double))
+    _c(L.kv_last_error, ctypes.c_char_p)
+    _c(L.kvattn_abi_version, i32)
+    _c(L.kvattn_decode_workspace_bytes, sz, i32, i32, i32, i32)
+    _c(L.kvattn_decode_split_tokens, i32, i32)
+    _c(L.kvattn_decode, i32, vp, vp, i32, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
+       i32, vp, sz, vp)
+    _c(L.kvattn_prefill_workspace_bytes, sz, i32, i32, i32, i32)
+    _c(L.kvattn_prefill_chunk, i32, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+       i32, i32, i32, f32, i32, vp, sz, vp)
+    _c(L.kvpool_granularity, i32, i32, ctypes.POINTER(ctypes.c_size_t))
+    _c(L.kvpool_create, i32, i32, i32, sz, sz, ctypes.POINTER(vp))
+    _c(L.kvpool_layer_ptr, i32, vp, i32, ctypes.POINTER(vp))
+    _c(L.kvpool_is_committed, i32, vp)
+    _c(L.kvpool_commit_elastic, i32, vp, dp)
+    _c(L.kvpool_decommit_elastic, i32, vp, dp)
+    _c(L.kvpool_sizes, i32, vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_size_t),
+       ctypes.POINTER(ctypes.c_size_t))
+    _c(L.kvpool_last_toggle_breakdown, i32, vp, dp, dp, dp, dp, dp)
+    _c(L.kvpool_destroy, None, vp)
+    _c(L.kvattn_trace_begin, i32, ctypes.POINTER(vp), i32)
+    _c(L.kvattn_trace_end, i32, ctypes.POINTER(i32))
+    _c(L.kvattn_trace_kernel_name, ctypes.c_char_p, i32)
+    _lib = L
+    return L
+
+
+def declared_symbols() -> list:
+    """Function names declared in include/kvattn.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kv\w+)\s*\(", text)))
+
+
+def last_error() -> str:
+    return lib().kv_last_error().decode()
+
+
+def check(rc: int) -> None:
+    if rc != KV_OK:
+        raise KvAttnError(rc, last_error())
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return KV_BF16
+    if t == torch.float32:
+        return KV_F32
+    raise ValueError(f"unsupported dtype {t}")
+
+
+def _ptr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _require_cuda(*ts):
+    for t in ts:
+        if isinstance(t, torch.Tensor) and not t.is_cuda:
+            raise ValueError("tensors must be on the GPU")
+
+
+def decode_workspace_bytes(num_seqs: int, num_q_heads: int, head_dim: int, max_seq_len: int) -> int:
+    return int(lib().kvattn_decode_workspace_bytes(num_seqs, num_q_heads, head_dim, max_seq_len))
+
+
+def decode_split_tokens(max_seq_len: int) -> int:
+    return int(lib().kvattn_decode_split_tokens(max_seq_len))
+
+
+def prefill_workspace_bytes(num_seqs: int, total_q_tokens: int, num_q_heads: int,
+                            head_dim: int) -> int:
+    return int(lib().kvattn_prefill_workspace_bytes(num_seqs, total_q_tokens, num_q_heads,
+                                                    head_dim))
+
+
+def workspace(nbytes: int, device=None) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8,
+                       device=device if device is not None else "cuda")
+
+
+def decode(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor,
+           seq_lens: torch.Tensor, *, num_kv_heads: int, max_seq_len: int,
+           block_size: int = 16, scale: Optional[float] = None,
+           out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    """Paged decode: ``q`` [B, Hq, d] -> out [B, Hq, d] (same dtype).
+
+    ``kv_layer`` is a tensor or a device address of the layer base.
+    """
+    B, Hq, d = q.shape
+    _require_cuda(q, block_table, seq_lens)
+    if out is None:
+        out = torch.empty_like(q)
+    if ws is None:
+        ws = workspace(decode_workspace_bytes(B, Hq, d, max_seq_len), q.device)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    rc = lib().kvattn_decode(_ptr(q), _ptr(kv_layer), int(num_blocks), _ptr(block_table),
+                             _ptr(seq_lens), _ptr(out), B, Hq, int(num_kv_heads), d,
+                             int(block_size), int(block_table.shape[1]), int(max_seq_len),
+                             float(scale), _dtype_code(q.dtype), _ptr(ws), ws.numel(),
+                             _stream(stream))
+    check(rc)
+    return out
+
+
+def prefill_chunk(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor,
+                  seq_lens: torch.Tensor, cu_seqlens_q: torch.Tensor, *, num_kv_heads: int,
+                  max_seq_len: int, max_num_batched_tokens: Optional[int] = None,
+                  block_size: int = 16, scale: Optional[float] = None,
+                  out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                  stream=None) -> torch.Tensor:
+    """Chunked prefill: ``q`` [T, Hq, d] bf16, chunks given by ``cu_seqlens_q``."""
+    T, Hq, d = q.shape
+    _require_cuda(q, block_table, seq_lens, cu_seqlens_q)
+    B = int(seq_lens.shape[0])
+    if out is None:
+        out = torch.empty_like(q)
+    if ws is None:
+        ws = workspace(prefill_workspace_bytes(B, T, Hq, d), q.device)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    budget = T if max_num_batched_tokens is None else int(max_num_batched_tokens)
+    rc = lib().kvattn_prefill_chunk(_ptr(q), _ptr(kv_layer), int(num_blocks), _ptr(block_table),
+                                    _ptr(seq_lens), _ptr(cu_seqlens_q), _ptr(out), B, T, budget,
+                                    Hq, int(num_kv_heads), d, int(block_size),
+                                    int(block_table.shape[1]), int(max_seq_len), float(scale),
+                                    _dtype_code(q.dtype), _ptr(ws), ws.numel(), _stream(stream))
+    check(rc)
+    return out
+
+
+class KernelTrace:
+    """Per-kernel HIP-event timing of the library's launches on this thread.
+
+    ``with KernelTrace(n) as tr: ...`` then ``tr.durations()`` gives a list of
+    (kernel name, milliseconds) for the traced launches."""
+
+    def __init__(self, max_kernels: int):
+        self.events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * max_kernels)]
+        for e in self.events:
+            e.record()          # materialise the underlying hipEvent_t
+        torch.cuda.synchronize()
+        self._arr = (ctypes.c_void_p * len(self.events))(*[e.cuda_event for e in self.events])
+        self.used = 0
+        self.names = []
+
+    def __enter__(self):
+        check(lib().kvattn_trace_begin(self._arr, len(self.events)))
+        return self
+
+    def __exit__(self, *exc):
+        n = ctypes.c_int()
+        check(lib().kvattn_trace_end(ctypes.byref(n)))
+        self.used = n.value
+        self.names = [lib().kvattn_trace_kernel_name(i).decode() for i in range(self.used // 2)]
+        return False
+
+    def durations(self):
+        torch.cuda.synchronize()
+        return [(self.names[i], self.events[2 * i].elapsed_time(self.events[2 * i + 1]))
+                for i in range(self.used // 2)]
+
+
+class _DeviceBytes:
+    """A raw device range exposed to torch through __cuda_array_interface__."""
+
+    def __init__(self, ptr: int, nbytes: int):
+        self.__cuda_array_interface__ = {"shape": (int(nbytes),), "typestr": "|u1",
+                                         "data": (int(ptr), False), "version": 3,
+                                         "strides": None}
+
+
+def device_view(ptr: int, nbytes: int, dtype: torch.dtype = torch.uint8,
+                device: int = 0) -> torch.Tensor:
+    """A torch tensor over ``nbytes`` of device memory at ``ptr`` (no copy).
+    The memory stays owned by whoever allocated it."""
+    with torch.cuda.device(device):
+        t = torch.as_tensor(_DeviceBytes(ptr, nbytes), device=f"cuda:{device}")
+    return t.view(dtype)
+
+
+class ElasticPool:
+    """Per-layer KV ranges of base + elastic bytes (kvpool_* in the C ABI)."""
+
+    def __init__(self, num_layers: int, base_bytes: int, elastic_bytes: int, device: int = 0):
+        L = lib()
+        h = ctypes.c_void_p()
+        check(L.kvpool_create(device, num_layers, base_bytes, elastic_bytes, ctypes.byref(h)))
+        self._h = h
+        self.device = device
+        self.num_layers = num_layers
+        self.base_bytes = base_bytes
+        self.elastic_bytes = elastic_bytes
+
+    @staticmethod
+    def granularity(device: int = 0) -> int:
+        g = ctypes.c_size_t()
+        check(lib().kvpool_granularity(device, ctypes.byref(g)))
+        return int(g.value)
+
+    def layer_ptr(self, layer: int) -> int:
+        p = ctypes.c_void_p()
+        check(lib().kvpool_layer_ptr(self._h, layer, ctypes.byref(p)))
+        return int(p.value)
+
+    def layer_view(self, layer: int, committed_part: bool = True,
+                   dtype: torch.dtype = torch.uint8) -> torch.Tensor:
+        """torch view of a layer: base only, or base + elastic (must be committed)."""
+        n = self.base_bytes + (self.elastic_bytes if committed_part else 0)
+        if committed_part and self.elastic_bytes and not self.is_committed:
+            raise KvAttnError(KV_ERR_STATE, "elastic range is not committed")
+        return device_view(self.layer_ptr(layer), n, dtype, self.device)
+
+    @property
+    def is_committed(self) -> bool:
+        rc = lib().kvpool_is_committed(self._h)
+        if rc < 0:
+            check(rc)
+        return rc == 1
+
+    def commit(self, empty_cache: bool = True) -> float:
+        """Commit the elastic sub-ranges; returns host wall ms of the commit call.
+        The torch caching allocator is emptied first so memory it holds from
+        earlier work is free for the physical handles."""
+        if empty_cache:
+            torch.cuda.empty_cache()
+        ms = ctypes.c_double()
+        check(lib().kvpool_commit_elastic(self._h, ctypes.byref(ms)))
+        return ms.value
+
+    def decommit(self) -> float:
+        ms = ctypes.c_double()
+        check(lib().kvpool_decommit_elastic(self._h, ctypes.byref(ms)))
+        return ms.value
+
+    def last_breakdown(self) -> dict:
+        v = [ctypes.c_double() for _ in range(5)]
+        check(lib().kvpool_last_toggle_breakdown(self._h, *[ctypes.byref(x) for x in v]))
+        return dict(zip(["create_ms", "map_ms", "access_ms", "sync_ms", "unmap_ms"],
+                        [x.value for x in v]))
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            lib().kvpool_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,115 @@
+"""Chunked-prefill parity: the HIP MFMA kernel through the C ABI against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+from workloads import config_spec, make_batch, make_batch_from_lens
+from tests.gpu_helpers import (Dev, assert_parity, f64, oracle_decode, oracle_prefill,
+                               oracle_rows, require_gpu, say)
+
+pytestmark = pytest.mark.gpu
+
+MIXED_L = [37, 100, 300, 513, 1, 64, 1000, 129, 2048]
+MIXED_N = [37, 20, 1, 257, 1, 16, 300, 65, 2048]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (4, 1)])
+def test_mixed_chunks_full(hq, hkv):
+    b = make_batch_from_lens(MIXED_L, MIXED_N, dtype="bf16", num_q_heads=hq, num_kv_heads=hkv,
+                             head_dim=128, block_size=16, seed=31)
+    say("prefill mixed", hq, hkv)
+    out = Dev(b).prefill()
+    torch.cuda.synchronize()
+    assert_parity(out, oracle_prefill(b), "bf16", f"mixed {hq}/{hkv}")
+
+
+def test_first_row_is_v0_exactly():
+    b = make_batch_from_lens([70], [70], dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=3, keep_contig=True)
+    say("prefill first row")
+    out = Dev(b).prefill().cpu()
+    want = b.v_contig[0][0].repeat_interleave(4, dim=0)
+    assert torch.equal(out[0].view(torch.int16), want.view(torch.int16))
+
+
+def test_causality_bitwise():
+    """Changing K/V after position p leaves rows up to p unchanged bit for bit."""
+    b = make_batch_from_lens([700], [700], dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=4)
+    d = Dev(b)
+    say("prefill causality")
+    ref = d.prefill().clone()
+    p = 450
+    tile = b.block_size * b.head_dim
+    layer = d.kv.view(b.num_blocks, 2, b.num_kv_heads, tile)
+    for blk in b.block_table[0, (p + 1 + 15) // 16: (700 + 15) // 16]:
+        layer[int(blk)] = 3.0
+    # the partial block holding p + 1 .. : rewrite the slots after p
+    blk = int(b.block_table[0, (p + 1) // 16])
+    kt = layer[blk, 0].view(b.num_kv_heads, 16, 16, 8)
+    vt = layer[blk, 1].view(b.num_kv_heads, 128, 16)
+    for t in range(p + 1, (p // 16 + 1) * 16):
+        kt[:, :, t % 16, :] = -2.0
+        vt[:, :, t % 16] = 5.0
+    got = d.prefill()
+    torch.cuda.synchronize()
+    assert torch.equal(got[:p + 1].view(torch.int16), ref[:p + 1].view(torch.int16))
+    assert not torch.equal(got[p + 1:], ref[p + 1:])
+
+
+def test_config4_chunk_equivalence():
+    """One 32768-token chunk versus four 8192-token chunks over the same cache:
+    both match the oracle, and the row tiling makes them bitwise equal."""
+    b = make_batch(config_spec(4))
+    d = Dev(b)
+    say("prefill config4 whole")
+    whole = d.prefill(max_num_batched_tokens=32768)
+    parts = []
+    for k in range(4):
+        say("prefill config4 chunk", k)
+        q = d.q[8192 * k: 8192 * (k + 1)]
+        sl = torch.tensor([8192 * (k + 1)], dtype=torch.int32, device="cuda")
+        cu = torch.tensor([0, 8192], dtype=torch.int32, device="cuda")
+        import paper_2608_23658_amd.kvattn as K
+        parts.append(K.prefill_chunk(q, d.kv, b.num_blocks, d.bt, sl, cu, num_kv_heads=8,
+                                     max_seq_len=32768, max_num_batched_tokens=8192,
+                                     scale=b.scale))
+    chunked = torch.cat(parts)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    rows = sorted(set([0, 1, 63, 64, 8191, 8192, 16383, 24576, 32767]
+                      + rng.choice(32768, 16, replace=False).tolist()))
+    ref = oracle_rows(b, rows)
+    assert_parity(f64(whole)[rows], ref, "bf16", "config4 whole, sampled rows")
+    assert_parity(f64(chunked)[rows], ref, "bf16", "config4 4x8192, sampled rows")
+    assert torch.equal(whole.view(torch.int16), chunked.view(torch.int16))
+
+
+def test_config3_mixed_step():
+    """The last 8192-token chunk of a 32768-token prompt plus 128 decode
+    sequences: as one unified call, and as a prefill call plus a decode call."""
+    b = make_batch(config_spec(3))
+    d = Dev(b)
+    say("prefill config3 unified")
+    uni = d.prefill(max_num_batched_tokens=8192 + 128)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(2)
+    rows = sorted(set([0, 1, 4095, 8191] + rng.choice(8192, 8, replace=False).tolist()
+                      + (8192 + rng.choice(128, 8, replace=False)).tolist()))
+    ref = oracle_rows(b, rows)
+    assert_parity(f64(uni)[rows], ref, "bf16", "config3 unified")
+    # decode part alone through the decode kernel
+    import paper_2608_23658_amd.kvattn as K
+    qd = d.q[8192:]
+    say("decode config3 part")
+    dec = K.decode(qd, d.kv, b.num_blocks, d.bt[1:], d.sl[1:], num_kv_heads=8,
+                   max_seq_len=b.max_seq_len, scale=b.scale)
+    torch.cuda.synchronize()
+    drows = [r for r in rows if r >= 8192]
+    assert_parity(f64(dec)[[r - 8192 for r in drows]], ref[[rows.index(r) for r in drows]],
+                  "bf16", "config3 decode part")

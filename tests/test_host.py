@@ -1,0 +1,149 @@
+"""Host-side logic that needs no GPU: the C ABI loads and exports what the
+header declares, argument checks fail before any launch, workspace sizing,
+and the algorithmic work counters against closed forms and the paper's
+figures."""
+import ctypes
+import json
+import os
+
+import numpy as np
+import pytest
+
+import paper_2608_23658_amd.kvattn as K
+from paper_2608_23658_amd import work
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return K.lib()
+
+
+def test_library_exports_every_declared_symbol(L):
+    names = K.declared_symbols()
+    assert len(names) >= 16
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.kvattn_abi_version() == 1
+
+
+# fake, 16-byte-aligned non-null addresses: every call below must be rejected
+# by the host checks, before anything is launched
+A = 1 << 20
+
+
+def _decode(L, **kw):
+    a = dict(q=A, kv=A, nb=100, bt=A, sl=A, out=A, B=4, hq=32, hkv=8, d=128, bs=16, mb=10,
+             msl=160, scale=0.1, dt=K.KV_BF16, ws=A, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return L.kvattn_decode(a["q"], a["kv"], a["nb"], a["bt"], a["sl"], a["out"], a["B"], a["hq"],
+                           a["hkv"], a["d"], a["bs"], a["mb"], a["msl"], a["scale"], a["dt"],
+                           a["ws"], a["wsb"], a["stream"])
+
+
+def _prefill(L, **kw):
+    a = dict(q=A, kv=A, nb=100, bt=A, sl=A, cu=A, out=A, B=2, T=100, budget=128, hq=32, hkv=8,
+             d=128, bs=16, mb=10, msl=160, scale=0.1, dt=K.KV_BF16, ws=A, wsb=1 << 20,
+             stream=None)
+    a.update(kw)
+    return L.kvattn_prefill_chunk(a["q"], a["kv"], a["nb"], a["bt"], a["sl"], a["cu"], a["out"],
+                                  a["B"], a["T"], a["budget"], a["hq"], a["hkv"], a["d"], a["bs"],
+                                  a["mb"], a["msl"], a["scale"], a["dt"], a["ws"], a["wsb"],
+                                  a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=96), K.KV_ERR_UNSUPPORTED),
+    (dict(d=128, dt=K.KV_F32), K.KV_ERR_UNSUPPORTED),
+    (dict(hq=24, hkv=8), K.KV_ERR_UNSUPPORTED),          # group of 3
+    (dict(hq=30, hkv=8), K.KV_ERR_INVALID),
+    (dict(bs=32), K.KV_ERR_UNSUPPORTED),
+    (dict(dt=7), K.KV_ERR_INVALID),
+    (dict(msl=161), K.KV_ERR_INVALID),                   # > max_blocks * block_size
+    (dict(nb=0), K.KV_ERR_INVALID),
+    (dict(q=A + 8), K.KV_ERR_INVALID),                   # misaligned
+    (dict(out=0), K.KV_ERR_INVALID),
+    (dict(wsb=100), K.KV_ERR_INVALID),                   # workspace too small
+    (dict(scale=float("inf")), K.KV_ERR_INVALID),
+    (dict(B=-1), K.KV_ERR_INVALID),
+])
+def test_decode_argument_checks(L, kw, code):
+    assert _decode(L, **kw) == code
+    assert K.last_error().startswith("kvattn_decode")
+
+
+def test_decode_empty_batch_is_ok(L):
+    assert _decode(L, B=0, q=0, out=0) == K.KV_OK
+    assert K.last_error() == ""
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=K.KV_F32), K.KV_ERR_UNSUPPORTED),
+    (dict(d=64), K.KV_ERR_UNSUPPORTED),
+    (dict(hq=64, hkv=8), K.KV_ERR_UNSUPPORTED),          # group of 8 is decode-only
+    (dict(T=200, budget=128), K.KV_ERR_INVALID),         # over max_num_batched_tokens
+    (dict(cu=0), K.KV_ERR_INVALID),
+    (dict(wsb=16), K.KV_ERR_INVALID),
+    (dict(msl=1000), K.KV_ERR_INVALID),
+])
+def test_prefill_argument_checks(L, kw, code):
+    assert _prefill(L, **kw) == code
+
+
+def test_workspace_sizes():
+    split = K.decode_split_tokens(4096)
+    assert split % 64 == 0 and split > 0
+    need = K.decode_workspace_bytes(256, 32, 128, 4096)
+    splits = -(-4096 // split)
+    assert need >= 256 * 32 * splits * (128 + 2) * 4
+    assert K.decode_workspace_bytes(-1, 32, 128, 4096) == 0
+    assert K.prefill_workspace_bytes(129, 8320, 32, 128) >= (8320 // 64 + 129) * 8
+
+
+def test_pool_rejects_bad_sizes_without_a_device(L):
+    h = ctypes.c_void_p()
+    assert L.kvpool_create(0, 0, 1 << 21, 1 << 21, ctypes.byref(h)) == K.KV_ERR_INVALID
+    assert L.kvpool_create(0, 2, 0, 0, ctypes.byref(h)) == K.KV_ERR_INVALID
+    assert not h.value
+    assert L.kvpool_commit_elastic(None, None) == K.KV_ERR_INVALID
+    assert L.kvpool_decommit_elastic(None, None) == K.KV_ERR_INVALID
+    assert L.kvpool_is_committed(None) == K.KV_ERR_INVALID
+    L.kvpool_destroy(None)
+
+
+def test_prefill_pairs_closed_forms_and_chunk_identity():
+    Lt = 32768
+    whole = work.prefill_pairs([Lt], [Lt])
+    assert whole == Lt * (Lt + 1) // 2 == 536_887_296
+    parts = [work.prefill_pairs([8192 * (k + 1)], [8192]) for k in range(4)]
+    assert sum(parts) == whole
+    assert parts == [33_558_528, 100_667_392, 167_776_256, 234_885_120]
+    # brute-force count on a small case
+    for L_, n in [(37, 37), (100, 20), (300, 1), (513, 257)]:
+        c = L_ - n
+        brute = sum(1 for i in range(n) for t in range(L_) if t <= c + i)
+        assert work.prefill_pairs([L_], [n]) == brute
+
+
+def test_flop_and_byte_counts():
+    # the last 8192-token chunk of a 32768-token prompt at 32 heads of 128
+    assert work.prefill_flops([32768], [8192], 32, 128) == 16384 * 234_885_120   # 3.848 TFLOP
+    assert work.prefill_flops([32768], [32768], 32, 128) == 4 * 128 * 32 * 536_887_296
+    # 4096 bytes of K+V per token per layer at 8 kv heads of 128 in bf16
+    assert work.decode_kv_bytes([1, 2, 3], 8, 128, 2) == 6 * 4096
+    b = work.decode_bytes([16, 17], 32, 8, 128, 2)
+    assert b == 33 * 4096 + 2 * 2 * 32 * 128 * 2 + 3 * 4 + 8
+
+
+def test_paper_figures_fixture():
+    """Figures the paper prints that bound the workloads (see the fixture's
+    citations): the decode share of the chunk budget and the toggle reserve."""
+    with open(os.path.join(GOLDEN, "paper_figures.json")) as f:
+        fig = json.load(f)
+    share = fig["decode_tokens_at_max_batch"] / fig["chunk_budget_small"]
+    assert abs(share - fig["decode_share_of_budget"]) < 0.005
+    # the 3 GiB reserve in 2 MiB granules spreads over 28 layers at ~56 granules each
+    per_layer = fig["reserve_gib"] * 1024 / fig["num_layers"]
+    assert 55 <= per_layer / fig["vmm_granularity_mib"] <= 57
+    assert fig["chunk_budget_large"] // fig["chunk_budget_small"] == 4
