@@ -64,7 +64,7 @@ using kvattn::set_error;
 namespace {
 
 constexpr int kAbiVersion = 1;
-constexpr int kDecodeSplitTokens = 512;
+constexpr int kDecodeSplitTokens = 1024;
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

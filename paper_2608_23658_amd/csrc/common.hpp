@@ -31,18 +31,53 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc) {
                                          __builtin_bit_cast(bf16x2_t, b), acc, false);
 }
 
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte load marked non-temporal: data read once streams past the caches.
+__device__ __forceinline__ uint4 load_nt(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Butterfly reductions across the 64 lanes of a wavefront.
+// DPP lane moves within rows of 16 lanes.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), kCtrl, 0xf, 0xf, false));
+}
+constexpr int kDppQuadSwap1 = 0xb1;       // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadSwap2 = 0x4e;       // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <-> 7 - i within each 8 lanes
+constexpr int kDppRowMirror = 0x140;      // lane i <-> 15 - i within each 16 lanes
+
+// Max / sum over all 64 lanes, result in every lane: four DPP steps inside
+// each row of 16 lanes, then the gfx950 row swaps (rows 0<->1 and 2<->3, then
+// the two halves of the wavefront).
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) x = fmaxf(x, __shfl_xor(x, o, kWave));
-  return x;
+  x = fmaxf(x, dpp_mov<kDppQuadSwap1>(x));
+  x = fmaxf(x, dpp_mov<kDppQuadSwap2>(x));
+  x = fmaxf(x, dpp_mov<kDppRowHalfMirror>(x));
+  x = fmaxf(x, dpp_mov<kDppRowMirror>(x));
+  const uint32_t u = __float_as_uint(x);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const uint32_t v = __float_as_uint(x);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) x += __shfl_xor(x, o, kWave);
-  return x;
+  x += dpp_mov<kDppQuadSwap1>(x);
+  x += dpp_mov<kDppQuadSwap2>(x);
+  x += dpp_mov<kDppRowHalfMirror>(x);
+  x += dpp_mov<kDppRowMirror>(x);
+  const uint32_t u = __float_as_uint(x);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const uint32_t v = __float_as_uint(x);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 }
 
 }  // namespace kvattn

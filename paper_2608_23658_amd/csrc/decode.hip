@@ -2,23 +2,31 @@
 // to its whole context, read through the block table (the paper, Section 3
 // "The contiguity constraint"; Section 5, decode is one token per sequence).
 //
-// One workgroup = one wavefront = one (split of the context, kv head,
-// sequence). The G query heads sharing the kv head are served by every K/V
-// byte read (grouped-query sharing). The wavefront walks its split in tiles
-// of 64 tokens (4 blocks of 16):
-//   * K: lane t owns token t of the tile. With the chunk-major K tile, the 16
+// One workgroup = one wavefront = one (kv head, sequence, split of the
+// context). The grid is one-dimensional with the kv head varying fastest and
+// the split slowest, so consecutive workgroups, which the dispatcher deals
+// round-robin to the 8 XCDs, carry equal work: putting the split first would
+// send split k of every sequence to XCD k and starve the XCDs that hold the
+// late splits only long sequences have. The G query heads sharing the kv
+// head are served by every K/V byte read (grouped-query sharing). The
+// wavefront walks its split in steps of 64 tokens (4 blocks of 16):
+//   * K: lane t owns token t of the step. With the chunk-major K tile, the 16
 //     lanes of one block read 256 contiguous bytes per 16-byte load, and each
 //     lane ends up holding its token's whole row, so q.k needs no cross-lane
-//     reduction. q is uniform and is read as scalar operands.
-//   * softmax: wavefront max per head, exp2 in the log2 domain, lane-local
-//     partial sums, one rescale of the accumulators per tile.
-//   * V: with the dim-major V tile, each 16-byte load is a 1 KiB contiguous
-//     stretch; lane l owns dim rows l / R (R = 16-byte chunks per row) and a
+//     reduction. q sits in LDS and every lane reads the same 16 bytes at a
+//     time (a broadcast).
+//   * softmax: wavefront max per head (DPP and lane-row swaps), exp2 in the
+//     log2 domain, lane-local partial sums, one rescale of the accumulators
+//     per step.
+//   * V: with the dim-major V tile each 16-byte load is a 1 KiB contiguous
+//     stretch (K and V are read once, so their loads are non-temporal); lane l owns dim rows l / R (R = 16-byte chunks per row) and a
 //     run of consecutive tokens, so for bf16 p.v is a bf16 dot2 over token
 //     pairs. p reaches those lanes through LDS.
-// Partials (m, l, o) of every split go to the workspace; a second kernel
-// merges them (log-sum-exp) in split order, so the result depends only on the
-// sequence's own length.
+// Only the last step of a split can hold slots past the sequence's length,
+// whose contents are arbitrary (possibly NaN); that step masks them. Partials
+// (m, l, o) of every split go to the workspace; a second kernel merges them
+// (log-sum-exp) in split order, so the result depends only on the sequence's
+// own length.
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -46,12 +54,13 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     const uint8_t* __restrict__ q, const uint8_t* __restrict__ kv, int num_blocks,
     const int* __restrict__ block_table, const int* __restrict__ seq_lens,
     uint8_t* __restrict__ out, float* __restrict__ ws_o, float2* __restrict__ ws_ml,
-    int num_q_heads, int num_kv_heads, int max_blocks, int max_seq_len, int split_tokens,
-    int max_splits, float scale_log2) {
+    int num_seqs, int num_q_heads, int num_kv_heads, int max_blocks, int max_seq_len,
+    int split_tokens, int max_splits, float scale_log2) {
   using S = DecodeShape<D, G, BF16>;
-  const int split = blockIdx.x;
-  const int g = blockIdx.y;
-  const int s = blockIdx.z;
+  const int wid = blockIdx.x;
+  const int g = wid % num_kv_heads;
+  const int s = (wid / num_kv_heads) % num_seqs;
+  const int split = wid / (num_kv_heads * num_seqs);
   const int lane = threadIdx.x;
   const int h0 = g * G;
   const size_t row_bytes = (size_t)D * S::kEsz;
@@ -72,8 +81,13 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
   const int t1 = min(L, t0 + split_tokens);
 
   __shared__ uint32_t p_lds[S::kPWords];
+  __shared__ uint4 q_lds[G * S::kKCh];
+  {
+    const uint4* qsrc = reinterpret_cast<const uint4*>(q + ((size_t)s * num_q_heads + h0) * row_bytes);
+    for (int i = lane; i < G * S::kKCh; i += kWave) q_lds[i] = qsrc[i];
+  }
+  __syncthreads();
 
-  const uint4* qv = reinterpret_cast<const uint4*>(q + ((size_t)s * num_q_heads + h0) * row_bytes);
   const int* bt = block_table + (size_t)s * max_blocks;
   const size_t tile_bytes = (size_t)S::kTileElems * S::kEsz;
   const size_t head_off = (size_t)g * tile_bytes;
@@ -93,13 +107,16 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
   const int kr = lane % S::kBS;   // its slot
   const int vrc = lane % S::kR;   // this lane's chunk of a V dim row
 
+  // Steps of 64 tokens; in the last one (kTail) the step may end inside a
+  // block, so tokens at or past t1 are masked.
   for (int tb = t0; tb < t1; tb += S::kTile) {
+    const bool kTail = tb + S::kTile > t1;
     const int blk0 = tb / S::kBS;
     int bid[S::kTB];
 #pragma unroll
     for (int j = 0; j < S::kTB; ++j) {
       int id = -1;
-      if (tb + j * S::kBS < t1) {
+      if (!kTail || tb + j * S::kBS < t1) {
         id = bt[blk0 + j];
         if ((unsigned)id >= (unsigned)num_blocks) id = -1;
       }
@@ -108,14 +125,14 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     int my_b = bid[0];
 #pragma unroll
     for (int j = 1; j < S::kTB; ++j) my_b = (kj == j) ? bid[j] : my_b;
-    const bool kvalid = (tb + lane < t1) && (my_b >= 0);
+    const bool kvalid = (!kTail || tb + lane < t1) && (my_b >= 0);
 
-    // ---- loads: K rows (lane-per-token), V dim rows ----
+    // ---- loads: K rows (lane per token), V dim rows ----
     uint4 kreg[S::kKCh];
     if (kvalid) {
       const uint4* kp = reinterpret_cast<const uint4*>(kv + (size_t)my_b * block_bytes + head_off) + kr;
 #pragma unroll
-      for (int c = 0; c < S::kKCh; ++c) kreg[c] = kp[c * S::kBS];
+      for (int c = 0; c < S::kKCh; ++c) kreg[c] = load_nt(kp + c * S::kBS);
     } else {
 #pragma unroll
       for (int c = 0; c < S::kKCh; ++c) kreg[c] = make_uint4(0, 0, 0, 0);
@@ -126,7 +143,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
       if (bid[j] >= 0) {
         const uint4* vp = reinterpret_cast<const uint4*>(kv + (size_t)bid[j] * block_bytes + v_off) + lane;
 #pragma unroll
-        for (int i = 0; i < S::kVI; ++i) vreg[j][i] = vp[i * kWave];
+        for (int i = 0; i < S::kVI; ++i) vreg[j][i] = load_nt(vp + i * kWave);
       } else {
 #pragma unroll
         for (int i = 0; i < S::kVI; ++i) vreg[j][i] = make_uint4(0, 0, 0, 0);
@@ -134,10 +151,6 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     }
 
     // ---- scores: q . k for the G heads, lane-local ----
-    // q is re-read from the scalar cache every step: hiding the pointer from
-    // the optimiser keeps all G * D of it from being hoisted into SGPRs.
-    const uint4* qv_t = qv;
-    asm volatile("" : "+s"(qv_t));
     float sc[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) sc[h] = 0.f;
@@ -146,7 +159,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
       const uint4 k = kreg[c];
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const uint4 qc = qv_t[h * S::kKCh + c];
+        const uint4 qc = q_lds[h * S::kKCh + c];
         if constexpr (BF16) {
           float a = sc[h];
           a = dot2_bf16(k.x, qc.x, a);
@@ -191,7 +204,6 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     __syncthreads();
 
     // ---- p . v ----
-    const bool partial = (tb + S::kTile > t1);
 #pragma unroll
     for (int j = 0; j < S::kTB; ++j) {
       if (bid[j] < 0) continue;
@@ -213,7 +225,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
 #pragma unroll
         for (int i = 0; i < S::kVI; ++i) {
           uint4 v = vreg[j][i];
-          if (partial) {
+          if (kTail) {
             uint32_t vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -245,7 +257,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
           const uint4 v = vreg[j][i];
           float vf[4] = {__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
                          __uint_as_float(v.w)};
-          if (partial) {
+          if (kTail) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) vf[k] = (tok0 + k < t1) ? vf[k] : 0.f;
           }
@@ -348,16 +360,18 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(
 template <int D, int G, bool BF16>
 static hipError_t launch_decode_t(const DecodeArgs& a) {
   const int max_splits = (a.max_seq_len + a.split_tokens - 1) / a.split_tokens;
-  const int grid_x = max_splits > 0 ? max_splits : 1;
+  const int splits = max_splits > 0 ? max_splits : 1;
+  const long long blocks = (long long)splits * a.num_kv_heads * a.num_seqs;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   float* ws_o = reinterpret_cast<float*>(a.workspace);
   float2* ws_ml = reinterpret_cast<float2*>(static_cast<uint8_t*>(a.workspace) + a.ws_ml_offset);
-  dim3 grid(grid_x, a.num_kv_heads, a.num_seqs);
   trace_before(a.stream, "decode_split");
-  hipLaunchKernelGGL((decode_split_kernel<D, G, BF16>), grid, dim3(64), 0, a.stream,
-                     static_cast<const uint8_t*>(a.q), static_cast<const uint8_t*>(a.kv),
-                     a.num_blocks, a.block_table, a.seq_lens, static_cast<uint8_t*>(a.out), ws_o,
-                     ws_ml, a.num_q_heads, a.num_kv_heads, a.max_blocks, a.max_seq_len,
-                     a.split_tokens, grid_x, a.scale * kLog2e);
+  hipLaunchKernelGGL((decode_split_kernel<D, G, BF16>), dim3((unsigned)blocks), dim3(64), 0,
+                     a.stream, static_cast<const uint8_t*>(a.q),
+                     static_cast<const uint8_t*>(a.kv), a.num_blocks, a.block_table, a.seq_lens,
+                     static_cast<uint8_t*>(a.out), ws_o, ws_ml, a.num_seqs, a.num_q_heads,
+                     a.num_kv_heads, a.max_blocks, a.max_seq_len, a.split_tokens, splits,
+                     a.scale * kLog2e);
   trace_after(a.stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_splits <= 1) return e;
@@ -366,7 +380,7 @@ static hipError_t launch_decode_t(const DecodeArgs& a) {
   hipLaunchKernelGGL((decode_combine_kernel<D, BF16>), dim3((pairs + 3) / 4), dim3(256), 0,
                      a.stream, ws_o, ws_ml, a.seq_lens, static_cast<uint8_t*>(a.out),
                      a.num_seqs, a.num_q_heads, a.max_blocks, a.max_seq_len, a.split_tokens,
-                     grid_x);
+                     splits);
   trace_after(a.stream);
   return hipGetLastError();
 }

@@ -5,22 +5,31 @@
 //
 // Work tile = (kv head g, 64 * 4 / G consecutive new rows of one sequence).
 // A workgroup of 4 wavefronts owns one tile: wave w serves query head
-// g * G + w % G over 64 rows. K/V tiles of 64 keys (4 blocks) are gathered
-// through the block table into LDS once per workgroup and shared by the G
-// query heads of the group.
+// g * G + w % G over 64 rows (two row tiles of 32). K/V steps of 64 keys (4
+// blocks) are gathered through the block table into double-buffered LDS once
+// per workgroup and shared by the G query heads of the group.
 //
-// Per wave and 64-key step, with v_mfma_f32_16x16x32_bf16:
-//   S^T[key][row] = K[key][:] . Q[row][:]   A = K rows straight from the
-//       chunk-major K tile (16-byte chunk c of slot r at (c * 16 + r) * 16),
-//       B = Q^T held in registers for the whole kernel;
-//   softmax over keys in the log2 domain: in the S^T accumulator layout every
-//       lane holds 4 keys of one query row, so the row max needs 2 shuffles
-//       and the rescale of O^T is lane-local;
-//   O^T[d][row] += V^T[d][key] P^T[key][row]   A = 8-byte runs of the
-//       dim-major V tile, B = the bf16 P values already in the lane that
-//       produced them (keys 4j..4j+3 of two consecutive blocks).
-// The causal mask (bottom-right: row i at position L - n + i sees keys
-// 0 .. L - n + i) is applied only on steps that reach the diagonal.
+// Per wave and step, with v_mfma_f32_32x32x16_bf16 (four independent
+// accumulator chains are enough to keep it busy, where the 16x16x32 form
+// needs sixteen):
+//   S^T[key][row] = K[key][:] . Q[row][:]   A = K rows read from the
+//       chunk-major K tile, B = Q^T held in registers for the whole kernel.
+//       The A rows of a 32-key tile are loaded in a permuted key order so
+//       that the accumulator of each lane ends up holding 8 consecutive keys
+//       of each of the two blocks for one query row;
+//   softmax over keys in the log2 domain: a row's 64 scores live in two
+//       lanes (l and l + 32), so the row max needs one exchange; the row
+//       state is lane-local. The running max is only moved, and O^T and the
+//       row sum rescaled, when a row's max grows by more than 2^8: the
+//       exponentials stay below 256, which bf16 P and fp32 accumulation hold;
+//   O^T[d][row] += V^T[d][key] P^T[key][row]   A = 16-byte runs of the
+//       dim-major V tile, B = the bf16 P values of 8 consecutive keys of one
+//       block, already in the lane that produced them.
+// V rows are stored in LDS with their two 16-byte halves swapped on every
+// other group of 8 rows, so the A reads of 16 rows hit 16 distinct bank
+// groups. The causal mask (bottom-right: row i at position L - n + i sees
+// keys 0 .. L - n + i) is applied only on steps that reach the diagonal or
+// the end of the sequence.
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -31,14 +40,15 @@ namespace {
 
 constexpr int kD = 128;
 constexpr int kBS = 16;
-constexpr int kKeys = 64;          // keys per step
-constexpr int kStepBlocks = 4;     // blocks per step
+constexpr int kKeys = 64;                  // keys per step
+constexpr int kStepBlocks = 4;             // blocks per step
 constexpr int kTileBytes = kBS * kD * 2;   // one (block, K/V, head) tile: 4 KiB
+constexpr float kLazyRescale = 8.f;        // log2 headroom before the max moves
 
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+__device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 }  // namespace
@@ -118,36 +128,39 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int* bt = block_table + (size_t)s * max_blocks;
   const int qstride = num_q_heads * kD;
 
-  // ---- Q^T operands for the wave's 64 rows (4 groups of 16) ----
-  const int lr = lane % 16;     // row within a group / key-or-dim index within a 16-tile
-  const int lq = lane / 16;     // quarter: which 8-wide k slice / which 4 accumulator rows
-  bf16x8_t qb[4][4];
+  const int lm = lane % 32;     // MFMA row / column index of this lane
+  const int lh = lane / 32;     // which 8-wide half of the 16-wide k slice
+  // Key permutation of the S^T rows: A row m = 8a + 4b + e holds key
+  // 16 (a / 2) + 8 b + 4 (a % 2) + e of the 32-key tile, so accumulator
+  // element i of lane l is key 16 (i / 8) + 8 (l / 32) + i % 8.
+  const int ka = lm / 8, kb4 = (lm / 4) % 2, ke = lm % 4;
+  const int k_blk = ka / 2;                              // block within the key tile
+  const int k_slot = 8 * kb4 + 4 * (ka % 2) + ke;        // slot within the block
+
+  // ---- Q^T operands for the wave's 64 rows (2 row tiles of 32) ----
+  bf16x8_t qb[2][8];
 #pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    const int r = row0 + rg * 16 + lr;
+  for (int rt = 0; rt < 2; ++rt) {
+    const int r = row0 + rt * 32 + lm;
 #pragma unroll
-    for (int ds = 0; ds < 4; ++ds) {
-      if (r < n) {
-        const uint4 v = *reinterpret_cast<const uint4*>(
-            q + (size_t)(cu0 + r) * qstride + (size_t)h * kD + ds * 32 + lq * 8);
-        qb[rg][ds] = __builtin_bit_cast(bf16x8_t, v);
-      } else {
-        qb[rg][ds] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
-      }
+    for (int ks = 0; ks < 8; ++ks) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (r < n)
+        v = *reinterpret_cast<const uint4*>(q + (size_t)(cu0 + r) * qstride + (size_t)h * kD +
+                                           ks * 16 + lh * 8);
+      qb[rt][ks] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 
-  f32x4_t oacc[8][4];
+  f32x16_t oacc[4][2];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt)
+  for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int rg = 0; rg < 4; ++rg) oacc[dt][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run[4], l_run[4];
+    for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    m_run[rg] = -INFINITY;
-    l_run[rg] = 0.f;
-  }
+      for (int i = 0; i < 16; ++i) oacc[dt][rt][i] = 0.f;
+  float m_ref[2] = {-INFINITY, -INFINITY};   // reference max of each row (log2 domain)
+  float l_run[2] = {0.f, 0.f};               // lane-partial row sums
 
   // ---- gather of one 64-key step into registers: 8 x 16 bytes per thread ----
   uint4 pre[2 * kStepBlocks];
@@ -171,6 +184,10 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       }
     }
   };
+  // V dim row tid / 2, half tid % 2 (slots 8 * (tid % 2) .. + 7); stored at
+  // the swizzled half. Slots at or past L are zeroed (their bytes may be NaN).
+  const int vrow = tid / 2, vhalf = tid % 2;
+  const int v_lds = vrow * 32 + ((vhalf ^ ((vrow >> 3) & 1)) * 16);
   auto store_step = [&](int buf, int step) {
     const int kbase = step * kKeys;
     const bool tail = kbase + kKeys > L;
@@ -178,8 +195,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     for (int kb = 0; kb < kStepBlocks; ++kb) {
       uint4 v = pre[kb * 2 + 1];
       if (tail) {
-        // V dim row tid / 2, slots 8 * (tid % 2) .. + 7: zero slots at or past L
-        const int key = kbase + kb * kBS + 8 * (tid % 2);
+        const int key = kbase + kb * kBS + 8 * vhalf;
         uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -190,7 +206,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
         v = make_uint4(w[0], w[1], w[2], w[3]);
       }
       *reinterpret_cast<uint4*>(&lds[buf][0][kb][tid * 16]) = pre[kb * 2 + 0];
-      *reinterpret_cast<uint4*>(&lds[buf][1][kb][tid * 16]) = v;
+      *reinterpret_cast<uint4*>(&lds[buf][1][kb][v_lds]) = v;
     }
   };
 
@@ -201,86 +217,105 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   __syncthreads();
 
   const int wave_pos0 = c + row0;   // position of the wave's first row
+  const int v_read = lm * 32 + ((lh ^ ((lm >> 3) & 1)) * 16);
   for (int step = 0; step < nsteps; ++step) {
     const int buf = step & 1;
     if (step + 1 < nsteps) load_step(step + 1);
     const int kbase = step * kKeys;
 
-    // ---- S^T = K Q^T ----
-    f32x4_t sacc[kStepBlocks][4];
+    // ---- S^T = K Q^T: 2 key tiles x 2 row tiles, 8 k-steps of 16 dims ----
+    f32x16_t sacc[2][2];
 #pragma unroll
-    for (int kb = 0; kb < kStepBlocks; ++kb)
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) sacc[kb][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sacc[kt][rt][i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const int chunk = 2 * ks + lh;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
+            &lds[buf][0][2 * kt + k_blk][(chunk * kBS + k_slot) * 16]);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) sacc[kt][rt] = mfma32(a, qb[rt][ks], sacc[kt][rt]);
+      }
+    }
+
+    // ---- online softmax per row (lane holds row lm of each row tile) ----
+    if ((kbase + kKeys - 1 > wave_pos0) || (kbase + kKeys > L)) {
+      // causal / length mask, only on steps that reach the diagonal or the end
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int kpos = kbase + kt * 32 + (i / 8) * 16 + lh * 8 + (i % 8);
+            const int qpos = wave_pos0 + rt * 32 + lm;
+            if (kpos > qpos || kpos >= L) sacc[kt][rt][i] = -INFINITY;
+          }
+    }
+    bf16x8_t pb[2][4];
+    float alpha[2];
+    float tmax[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][rt][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      tmax[rt] = mx * scale_log2;
+    }
+    // Move a row's reference max only when its scores outgrow it by 2^8.
+    const bool grow0 = tmax[0] > m_ref[0] + kLazyRescale;
+    const bool grow1 = tmax[1] > m_ref[1] + kLazyRescale;
+    const bool rescale = __builtin_amdgcn_ballot_w64(grow0 || grow1) != 0;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const bool grow = rt == 0 ? grow0 : grow1;
+      const float nref = grow ? tmax[rt] : m_ref[rt];
+      alpha[rt] = (m_ref[rt] == -INFINITY) ? 0.f : fast_exp2(m_ref[rt] - nref);
+      m_ref[rt] = nref;
+      const float ref = (nref == -INFINITY) ? 0.f : nref;
+      float psum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        float p[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          p[i] = fast_exp2(fmaf(sacc[kt][rt][i], scale_log2, -ref));
+          psum += p[i];
+        }
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const uint4 w = make_uint4(pack_bf16x2(p[8 * half + 0], p[8 * half + 1]),
+                                     pack_bf16x2(p[8 * half + 2], p[8 * half + 3]),
+                                     pack_bf16x2(p[8 * half + 4], p[8 * half + 5]),
+                                     pack_bf16x2(p[8 * half + 6], p[8 * half + 7]));
+          pb[rt][2 * kt + half] = __builtin_bit_cast(bf16x8_t, w);
+        }
+      }
+      l_run[rt] = l_run[rt] * alpha[rt] + psum;
+    }
+
+    // ---- O^T += V^T P^T: 4 dim tiles x 2 row tiles, one k-step per block ----
+    // (the rescale of O^T, when a row max moved, is folded in one 16-value
+    // accumulator at a time)
 #pragma unroll
     for (int kb = 0; kb < kStepBlocks; ++kb) {
 #pragma unroll
-      for (int ds = 0; ds < 4; ++ds) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&lds[buf][0][kb][(64 * ds + lane) * 16]);
+      for (int dt = 0; dt < 4; ++dt) {
+        const bf16x8_t a =
+            *reinterpret_cast<const bf16x8_t*>(&lds[buf][1][kb][dt * 32 * 32 + v_read]);
 #pragma unroll
-        for (int rg = 0; rg < 4; ++rg) sacc[kb][rg] = mfma16(a, qb[rg][ds], sacc[kb][rg]);
-      }
-    }
-
-    // ---- online softmax per row (lane holds row lr of each group) ----
-    const bool mask = (kbase + kKeys - 1 > wave_pos0) || (kbase + kKeys > L);
-    bf16x8_t pb[4][2];
-#pragma unroll
-    for (int rg = 0; rg < 4; ++rg) {
-      const int qpos = wave_pos0 + rg * 16 + lr;
-      float x[kStepBlocks][4];
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < kStepBlocks; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = sacc[kb][rg][i] * scale_log2;
-          if (mask) {
-            const int kpos = kbase + kb * kBS + lq * 4 + i;
-            v = (kpos > qpos || kpos >= L) ? -INFINITY : v;
-          }
-          x[kb][i] = v;
-          tmax = fmaxf(tmax, v);
+        for (int rt = 0; rt < 2; ++rt) {
+          if (kb == 0 && rescale) oacc[dt][rt] *= alpha[rt];
+          oacc[dt][rt] = mfma32(a, pb[rt][kb], oacc[dt][rt]);
         }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-      const float mn = fmaxf(m_run[rg], tmax);
-      const float ref = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = fast_exp2(m_run[rg] - ref);
-      m_run[rg] = mn;
-      float psum = 0.f;
-      float p[kStepBlocks][4];
-#pragma unroll
-      for (int kb = 0; kb < kStepBlocks; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          p[kb][i] = fast_exp2(x[kb][i] - ref);
-          psum += p[kb][i];
-        }
-      l_run[rg] = l_run[rg] * alpha + psum;
-#pragma unroll
-      for (int bp = 0; bp < 2; ++bp) {
-        const uint4 w = make_uint4(pack_bf16x2(p[2 * bp][0], p[2 * bp][1]),
-                                   pack_bf16x2(p[2 * bp][2], p[2 * bp][3]),
-                                   pack_bf16x2(p[2 * bp + 1][0], p[2 * bp + 1][1]),
-                                   pack_bf16x2(p[2 * bp + 1][2], p[2 * bp + 1][3]));
-        pb[rg][bp] = __builtin_bit_cast(bf16x8_t, w);
-      }
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) oacc[dt][rg] *= alpha;
-    }
-
-    // ---- O^T += V^T P^T ----
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-#pragma unroll
-      for (int bp = 0; bp < 2; ++bp) {
-        const int off = (dt * 16 + lr) * 32 + lq * 8;
-        const uint2 v0 = *reinterpret_cast<const uint2*>(&lds[buf][1][2 * bp][off]);
-        const uint2 v1 = *reinterpret_cast<const uint2*>(&lds[buf][1][2 * bp + 1][off]);
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) oacc[dt][rg] = mfma16(a, pb[rg][bp], oacc[dt][rg]);
       }
     }
 
@@ -288,22 +323,23 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     __syncthreads();
   }
 
-  // ---- normalise and write O (rows of this lane: lr of each group) ----
+  // ---- normalise and write O (this lane: row lm of each row tile) ----
 #pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    float lt = l_run[rg];
-    lt += __shfl_xor(lt, 16, kWave);
-    lt += __shfl_xor(lt, 32, kWave);
+  for (int rt = 0; rt < 2; ++rt) {
+    float lt = l_run[rt] + __shfl_xor(l_run[rt], 32, kWave);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int r = row0 + rg * 16 + lr;
+    const int r = row0 + rt * 32 + lm;
     if (r < n) {
       uint16_t* orow = out + (size_t)(cu0 + r) * qstride + (size_t)h * kD;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const f32x4_t o = oacc[dt][rg];
-        const uint2 w = make_uint2(pack_bf16x2(o[0] * inv, o[1] * inv),
-                                   pack_bf16x2(o[2] * inv, o[3] * inv));
-        *reinterpret_cast<uint2*>(orow + dt * 16 + lq * 4) = w;
+      for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const f32x16_t& o = oacc[dt][rt];
+          const uint2 w = make_uint2(pack_bf16x2(o[4 * a + 0] * inv, o[4 * a + 1] * inv),
+                                     pack_bf16x2(o[4 * a + 2] * inv, o[4 * a + 3] * inv));
+          *reinterpret_cast<uint2*>(orow + dt * 32 + a * 8 + lh * 4) = w;
+        }
       }
     }
   }
