@@ -39,8 +39,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
-                    choices=["all", "decode", "prefill", "mixed", "toggle"],
-                    help="'all' = headline decode plus the prefill, mixed-step and toggle legs")
+                    choices=["all", "decode", "prefill", "mixed", "toggle", "copy"],
+                    help="'all' = headline decode plus the prefill, mixed-step and toggle "
+                         "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
+                         "scales the HBM byte counters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
@@ -83,16 +85,46 @@ def timed(fn, steps, warmup, K, kernel):
     return t.ms / steps, means.get(kernel), means
 
 
-def roofline_hbm(bytes_per_launch, kernel_ms):
+PROFILES = os.path.join(ROOT, "profiles")
+COPY_BYTES = 2 << 30
+
+
+def measured_traffic(name):
+    """HBM bytes per launch from the counter summary in profiles/, or None if
+    there is none or the kernel's source changed since it was taken."""
+    from paper_2608_23658_amd.profiling import traffic_if_current
+    t = traffic_if_current(os.path.join(PROFILES, name), ROOT)
+    return None if t is None else int(t)
+
+
+def roofline_hbm(bytes_per_launch, kernel_ms, traffic=None):
     ach = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
 
 
-def roofline_mfma(flops_per_launch, kernel_ms):
+def roofline_mfma(flops_per_launch, kernel_ms, traffic=None):
     ach = flops_per_launch / (kernel_ms * 1e-3) / 1e12
     return {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+            "unit": "TFLOP/s", "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": traffic}
+
+
+def copy_leg(args):
+    """A plain elementwise copy of COPY_BYTES (read COPY_BYTES, write COPY_BYTES):
+    the known-size kernel whose byte counters calibrate the others."""
+    n = COPY_BYTES // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(max(1, args.warmup)):
+        torch.mul(src, 1.0, out=dst)
+    with Timer() as t:
+        for _ in range(args.steps):
+            torch.mul(src, 1.0, out=dst)
+    ms = t.ms / args.steps
+    log(f"copy: {ms:.3f} ms, {2 * COPY_BYTES / ms / 1e6:.0f} GB/s read+write")
+    return {"bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES, "ms": ms,
+            "gbs": 2 * COPY_BYTES / ms / 1e6}
 
 
 def decode_leg(args, K, work, wl):
@@ -120,7 +152,8 @@ def decode_leg(args, K, work, wl):
         "gbs": nbytes / (ms * 1e-3) / 1e9,
         "kv_gbs": kvb / (ms * 1e-3) / 1e9,
         "bytes_per_step": nbytes, "kernel_ms": means,
-        "roofline": roofline_hbm(nbytes, kern_ms),
+        "roofline": roofline_hbm(nbytes, kern_ms,
+                                 measured_traffic("traffic_decode_split_b256_l512_4096.txt")),
         "num_seqs": b.num_seqs, "sum_seq_len": int(b.seq_lens.sum()),
     }
     return res, b
@@ -154,7 +187,8 @@ def prefill_leg(args, K, work):
         log(f"prefill {name}: {ms:.3f} ms/call, {flops / ms / 1e9:.1f} TFLOP/s, kernels {means}")
         res[name] = {"ms_per_call": ms, "tflops": flops / (ms * 1e-3) / 1e12,
                      "flops_per_call": flops, "kernel_ms": means,
-                     "roofline": roofline_mfma(flops, kern_ms)}
+                     "roofline": roofline_mfma(flops, kern_ms, measured_traffic(
+                         f"traffic_prefill_{name}.txt"))}
     return res, b
 
 
@@ -307,6 +341,10 @@ def main():
         line["mixed_step"] = mixed_leg(args, K, work)
     if args.workload in ("all", "toggle"):
         line["elastic_toggle"] = toggle_leg(K)
+    if args.workload == "copy":
+        c = copy_leg(args)
+        line.update(value=round(c["gbs"], 1), unit="GB/s", ms_per_step=round(c["ms"], 5),
+                    config={"workload": "elementwise_copy_2GiB_f32"}, copy=c)
     if dec_batch is not None and not args.no_cpu_baseline:
         log("cpu baseline: oracle sample")
         line["cpu_baseline"] = cpu_baseline(dec_batch, work, args.cpu_seconds)
