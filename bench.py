@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
-                    choices=["all", "decode", "prefill", "mixed", "toggle", "copy"],
+                    choices=["all", "decode", "prefill", "mixed", "toggle", "elastic", "copy"],
                     help="'all' = headline decode plus the prefill, mixed-step and toggle "
                          "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
                          "scales the HBM byte counters")
@@ -262,6 +262,109 @@ def toggle_leg(K):
     return res
 
 
+def elastic_leg(args, K, work):
+    """Decode over 32 layers of an elastic pool (base 96768 + 1536 elastic
+    blocks of 64 KiB per layer, 3 GiB of elastic reserve in all), 512
+    sequences U[8192, 32768], one shared table with >= 15% elastic references.
+    States: committed; decommitted with the elastic references remapped onto
+    base ids (same reuse structure; num_blocks = base blocks, so nothing can
+    touch the unmapped range); recommitted with the elastic part refilled
+    (output must equal the committed one bit for bit); and a plain
+    torch-allocated copy of layer 0 as the control (against the pool's own
+    layer 0 read 32 times, which has the same one-layer footprint)."""
+    from workloads.configs import ELASTIC as E
+    from workloads.elastic import (elastic_queries, elastic_tables, fill_layer,
+                                   remap_elastic_to_base)
+    bf16 = torch.bfloat16
+    torch.cuda.empty_cache()
+    bb = E.block_bytes
+    base, el = E.base_blocks * bb, E.elastic_bytes_per_layer
+    nb_all = E.base_blocks + E.elastic_blocks
+    lens, bt_np, el_mask = elastic_tables(E)
+    bt = torch.from_numpy(bt_np).cuda()
+    bt_base = torch.from_numpy(remap_elastic_to_base(bt_np, E)).cuda()
+    sl = torch.from_numpy(lens).cuda()
+    q = elastic_queries(E).cuda()
+    msl = int(lens.max())
+    ws = K.workspace(K.decode_workspace_bytes(E.batch, E.num_q_heads, E.head_dim, msl))
+    outs = torch.empty(E.num_layers, E.batch, E.num_q_heads, E.head_dim, dtype=bf16,
+                       device="cuda")
+    reps = 3
+    log(f"elastic: pool of {E.num_layers} x ({base >> 20} MiB base + {el >> 20} MiB elastic)")
+    pool = K.ElasticPool(E.num_layers, base, el)
+    res = {"workload": E.name, "layers": E.num_layers, "base_blocks": E.base_blocks,
+           "elastic_blocks": E.elastic_blocks, "num_seqs": E.batch,
+           "sum_seq_len": int(lens.sum()),
+           "elastic_ref_fraction": float(el_mask.sum() / (bt_np >= 0).sum())}
+    try:
+        pool.commit()
+        for l in range(E.num_layers):
+            fill_layer(pool.layer_view(l, dtype=bf16), l, base // 2)
+        ptrs = [pool.layer_ptr(l) for l in range(E.num_layers)]
+
+        def sweep(table, nblocks, layers=None, src=None):
+            for l in (range(E.num_layers) if layers is None else layers):
+                K.decode(q, ptrs[l] if src is None else src, nblocks, table, sl,
+                         num_kv_heads=E.num_kv_heads, max_seq_len=msl, scale=E.scale,
+                         out=outs[l], ws=ws)
+
+        def per_layer_ms(table, nblocks, layers=None, src=None):
+            n = E.num_layers if layers is None else len(layers)
+            sweep(table, nblocks, layers, src)
+            with Timer() as t:
+                for _ in range(reps):
+                    sweep(table, nblocks, layers, src)
+            return t.ms / (reps * n)
+
+        committed = per_layer_ms(bt, nb_all)
+        ref = outs.clone()
+        log(f"elastic: committed {committed:.3f} ms/layer")
+        dec_ms = pool.decommit()
+        decommitted = per_layer_ms(bt_base, E.base_blocks)
+        log(f"elastic: decommitted {decommitted:.3f} ms/layer")
+        com_ms = pool.commit()
+        for l in range(E.num_layers):
+            fill_layer(pool.layer_view(l, dtype=bf16), l, base // 2, part="elastic")
+        sweep(bt, nb_all)
+        torch.cuda.synchronize()
+        bitwise = bool(torch.equal(outs.view(torch.int16), ref.view(torch.int16)))
+        recommitted = per_layer_ms(bt, nb_all)
+        log(f"elastic: recommitted {recommitted:.3f} ms/layer, bitwise equal {bitwise}")
+        # the footprint control: the pool's layer 0 read by all 32 calls of a
+        # sweep; then the same bytes in plain torch memory
+        pool_l0 = per_layer_ms(bt, nb_all, layers=[0] * E.num_layers)
+        ctl = torch.empty(base + el, dtype=torch.uint8, device="cuda")
+        ctl.copy_(pool.layer_view(0))
+        control = per_layer_ms(bt, nb_all, layers=[0] * E.num_layers, src=ctl.data_ptr())
+        ctl_equal = bool(torch.equal(outs[0].view(torch.int16), ref[0].view(torch.int16)))
+        del ctl
+        # toggle cycles on the full pool, no kernels in flight
+        cyc_c, cyc_d = [], []
+        for _ in range(12):
+            cyc_d.append(pool.decommit())
+            cyc_c.append(pool.commit(empty_cache=False))
+    finally:
+        pool.close()
+    nbytes = work.decode_bytes(lens, E.num_q_heads, E.num_kv_heads, E.head_dim, 2)
+    med = statistics.median
+    res.update({
+        "bytes_per_layer": nbytes,
+        "ms_per_layer": {"committed": committed, "decommitted": decommitted,
+                         "recommitted": recommitted, "pool_layer0_x32": pool_l0,
+                         "torch_layer0_x32": control},
+        "gbs_per_layer": {k: nbytes / (v * 1e-3) / 1e9 for k, v in
+                          (("committed", committed), ("decommitted", decommitted),
+                           ("recommitted", recommitted), ("pool_layer0_x32", pool_l0),
+                           ("torch_layer0_x32", control))},
+        "decommitted_vs_committed_pct": 100.0 * (decommitted / committed - 1.0),
+        "recommitted_bitwise_equal": bitwise, "control_bitwise_equal": ctl_equal,
+        "sweep_ms_committed": committed * E.num_layers,
+        "toggle_during_protocol_ms": {"decommit": dec_ms, "commit": com_ms},
+        "toggle_cycles_ms_median": {"decommit": med(cyc_d), "commit": med(cyc_c)},
+    })
+    return res
+
+
 def cpu_baseline(b, work, seconds):
     """The fp64 oracle on the first sequences of the decode batch, as many as
     fit in about `seconds` of wall time; reported in the headline's unit."""
@@ -341,6 +444,13 @@ def main():
         line["mixed_step"] = mixed_leg(args, K, work)
     if args.workload in ("all", "toggle"):
         line["elastic_toggle"] = toggle_leg(K)
+    if args.workload in ("all", "elastic"):
+        line["elastic_decode"] = elastic_leg(args, K, work)
+        if line["value"] is None:
+            e = line["elastic_decode"]
+            line.update(value=round(e["gbs_per_layer"]["committed"], 1), unit="GB/s",
+                        ms_per_step=round(e["ms_per_layer"]["committed"], 5),
+                        config={"workload": e["workload"]})
     if args.workload == "copy":
         c = copy_leg(args)
         line.update(value=round(c["gbs"], 1), unit="GB/s", ms_per_step=round(c["ms"], 5),
