@@ -31,6 +31,8 @@
 // keys 0 .. L - n + i) is applied only on steps that reach the diagonal or
 // the end of the sequence.
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -44,11 +46,31 @@ constexpr int kKeys = 64;                  // keys per step
 constexpr int kStepBlocks = 4;             // blocks per step
 constexpr int kTileBytes = kBS * kD * 2;   // one (block, K/V, head) tile: 4 KiB
 constexpr float kLazyRescale = 8.f;        // log2 headroom before the max moves
+constexpr int kBufs = 3;                   // LDS steps in the software pipeline
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// acc *= a on an accumulator that lives in AGPRs. The running output stays in
+// the accumulator registers the matrix instructions write; a plain vector
+// multiply would make the compiler carry it in VGPRs and copy it across on
+// every step, although the rescale itself is rare.
+__device__ __forceinline__ void scale_acc(f32x16_t& acc, float a) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float x = acc[i];
+    float t;
+    asm volatile(
+        "v_accvgpr_read_b32 %1, %0\n\t"
+        "v_mul_f32 %1, %1, %2\n\t"
+        "v_accvgpr_write_b32 %0, %1"
+        : "+a"(x), "=&v"(t)
+        : "v"(a));
+    acc[i] = x;
+  }
 }
 
 }  // namespace
@@ -107,7 +129,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int s = tl.x;
   const int q0 = tl.y;
   const int tid = threadIdx.x;
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform per wavefront
   const int lane = tid % kWave;
   const int h = g * G + wave % G;
   const int row0 = q0 + (wave / G) * 64;        // first row of this wave
@@ -120,7 +142,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int last_pos = min(c + q0 + wg_rows - 1, L - 1);
   const int nsteps = last_pos >= 0 ? last_pos / kKeys + 1 : 0;
 
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][kStepBlocks][kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kBufs][2][kStepBlocks][kTileBytes];
 
   const size_t block_bytes = 2 * (size_t)num_kv_heads * kTileBytes;
   const size_t k_off = (size_t)g * kTileBytes;
@@ -137,18 +159,18 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int k_blk = ka / 2;                              // block within the key tile
   const int k_slot = 8 * kb4 + 4 * (ka % 2) + ke;        // slot within the block
 
-  // ---- Q^T operands for the wave's 64 rows (2 row tiles of 32) ----
+  // ---- Q^T operands of the wave's two streams of 32 rows ----
   bf16x8_t qb[2][8];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const int r = row0 + rt * 32 + lm;
+  for (int r = 0; r < 2; ++r) {
+    const int row = row0 + r * 32 + lm;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (r < n)
-        v = *reinterpret_cast<const uint4*>(q + (size_t)(cu0 + r) * qstride + (size_t)h * kD +
-                                           ks * 16 + lh * 8);
-      qb[rt][ks] = __builtin_bit_cast(bf16x8_t, v);
+      if (row < n)
+        v = *reinterpret_cast<const uint4*>(q + (size_t)(cu0 + row) * qstride +
+                                           (size_t)h * kD + ks * 16 + lh * 8);
+      qb[r][ks] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 
@@ -156,81 +178,81 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int r = 0; r < 2; ++r)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[dt][rt][i] = 0.f;
+      for (int i = 0; i < 16; ++i) oacc[dt][r][i] = 0.f;
   float m_ref[2] = {-INFINITY, -INFINITY};   // reference max of each row (log2 domain)
   float l_run[2] = {0.f, 0.f};               // lane-partial row sums
 
-  // ---- gather of one 64-key step into registers: 8 x 16 bytes per thread ----
-  uint4 pre[2 * kStepBlocks];
+  // ---- gather of one 64-key step straight into LDS (global_load_lds, 16 B/lane) ----
+  // Each wavefront fills a contiguous 1 KiB quarter of every 4 KiB tile. K is
+  // copied as stored; for V the lane picks the global 16 bytes that belong at
+  // its swizzled LDS position (row tid / 2, half tid % 2 holds global half
+  // (tid % 2) ^ ((row >> 3) & 1)). A block past L or with an id outside
+  // [0, num_blocks) is replaced by block 0 (the host guarantees one exists);
+  // the returned bit mask (bit kb: block kb is real) lets the softmax mask its
+  // keys and patch_step zero its values.
+  const int vrow = tid / 2;
+  const int v_src = vrow * 32 + (((tid % 2) ^ ((vrow >> 3) & 1)) * 16);
   auto load_step = [&](int step) {
+    const int buf = step % kBufs;
     const int kbase = step * kKeys;
+    int bits = 0;
 #pragma unroll
     for (int kb = 0; kb < kStepBlocks; ++kb) {
       const int key0 = kbase + kb * kBS;
-      int id = -1;
-      if (key0 < L) {
-        id = bt[key0 / kBS];
-        if ((unsigned)id >= (unsigned)num_blocks) id = -1;
-      }
-      if (id >= 0) {
-        const uint8_t* base = kv + (size_t)id * block_bytes + tid * 16;
-        pre[kb * 2 + 0] = *reinterpret_cast<const uint4*>(base + k_off);
-        pre[kb * 2 + 1] = *reinterpret_cast<const uint4*>(base + v_off);
-      } else {
-        pre[kb * 2 + 0] = make_uint4(0, 0, 0, 0);
-        pre[kb * 2 + 1] = make_uint4(0, 0, 0, 0);
-      }
+      int id = key0 < L ? bt[key0 / kBS] : -1;
+      const bool ok = (unsigned)id < (unsigned)num_blocks;
+      bits |= ok ? (1 << kb) : 0;
+      const uint8_t* base = kv + (size_t)(ok ? id : 0) * block_bytes;
+      __builtin_amdgcn_global_load_lds(base + k_off + tid * 16, &lds[buf][0][kb][wave * 1024], 16,
+                                       0, 0);
+      __builtin_amdgcn_global_load_lds(base + v_off + v_src, &lds[buf][1][kb][wave * 1024], 16,
+                                       0, 0);
     }
+    return bits;
   };
-  // V dim row tid / 2, half tid % 2 (slots 8 * (tid % 2) .. + 7); stored at
-  // the swizzled half. Slots at or past L are zeroed (their bytes may be NaN).
-  const int vrow = tid / 2, vhalf = tid % 2;
-  const int v_lds = vrow * 32 + ((vhalf ^ ((vrow >> 3) & 1)) * 16);
-  auto store_step = [&](int buf, int step) {
+  // Zero the V slots of a landed step that must not contribute: blocks that
+  // are not real, and slots at or past L (their bytes may be NaN, and a zero
+  // weight times NaN is NaN). Called only when such slots exist.
+  auto patch_step = [&](int step, int bits) {
+    const int buf = step % kBufs;
     const int kbase = step * kKeys;
-    const bool tail = kbase + kKeys > L;
+    const int half_g = (tid % 2) ^ ((vrow >> 3) & 1);
 #pragma unroll
     for (int kb = 0; kb < kStepBlocks; ++kb) {
-      uint4 v = pre[kb * 2 + 1];
-      if (tail) {
-        const int key = kbase + kb * kBS + 8 * vhalf;
-        uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t lo = (key + 2 * k < L) ? 0x0000ffffu : 0u;
-          const uint32_t hi = (key + 2 * k + 1 < L) ? 0xffff0000u : 0u;
-          w[k] &= (lo | hi);
-        }
-        v = make_uint4(w[0], w[1], w[2], w[3]);
+      uint4* v = reinterpret_cast<uint4*>(&lds[buf][1][kb][tid * 16]);
+      if (!((bits >> kb) & 1)) {
+        *v = make_uint4(0, 0, 0, 0);
+        continue;
       }
-      *reinterpret_cast<uint4*>(&lds[buf][0][kb][tid * 16]) = pre[kb * 2 + 0];
-      *reinterpret_cast<uint4*>(&lds[buf][1][kb][v_lds]) = v;
+      const int key = kbase + kb * kBS + 8 * half_g;
+      if (key + 8 <= L) continue;
+      uint4 w4 = *v;
+      uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t lo = (key + 2 * k < L) ? 0x0000ffffu : 0u;
+        const uint32_t hi = (key + 2 * k + 1 < L) ? 0xffff0000u : 0u;
+        w[k] &= (lo | hi);
+      }
+      *v = make_uint4(w[0], w[1], w[2], w[3]);
     }
   };
-
-  if (nsteps > 0) {
-    load_step(0);
-    store_step(0, 0);
-  }
-  __syncthreads();
+  auto step_clean = [&](int step, int bits) { return bits == 0xf && (step + 1) * kKeys <= L; };
+  // All of this wave's direct-to-LDS loads have landed.
+  auto wait_loads = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
   const int wave_pos0 = c + row0;   // position of the wave's first row
   const int v_read = lm * 32 + ((lh ^ ((lm >> 3) & 1)) * 16);
-  for (int step = 0; step < nsteps; ++step) {
-    const int buf = step & 1;
-    if (step + 1 < nsteps) load_step(step + 1);
-    const int kbase = step * kKeys;
 
-    // ---- S^T = K Q^T: 2 key tiles x 2 row tiles, 8 k-steps of 16 dims ----
-    f32x16_t sacc[2][2];
+  // S^T of stream r for one step: 2 key tiles x 8 k-steps of 16 dims.
+  auto qk = [&](int r, int step, f32x16_t (&sa)[2]) {
+    const int buf = step % kBufs;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sacc[kt][rt][i] = 0.f;
+      for (int i = 0; i < 16; ++i) sa[kt][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
 #pragma unroll
@@ -238,89 +260,146 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
         const int chunk = 2 * ks + lh;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
             &lds[buf][0][2 * kt + k_blk][(chunk * kBS + k_slot) * 16]);
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt) sacc[kt][rt] = mfma32(a, qb[rt][ks], sacc[kt][rt]);
+        sa[kt] = mfma32(a, qb[r][ks], sa[kt]);
       }
     }
-
-    // ---- online softmax per row (lane holds row lm of each row tile) ----
-    if ((kbase + kKeys - 1 > wave_pos0) || (kbase + kKeys > L)) {
-      // causal / length mask, only on steps that reach the diagonal or the end
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int kpos = kbase + kt * 32 + (i / 8) * 16 + lh * 8 + (i % 8);
-            const int qpos = wave_pos0 + rt * 32 + lm;
-            if (kpos > qpos || kpos >= L) sacc[kt][rt][i] = -INFINITY;
-          }
-    }
-    bf16x8_t pb[2][4];
-    float alpha[2];
-    float tmax[2];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][rt][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      tmax[rt] = mx * scale_log2;
-    }
-    // Move a row's reference max only when its scores outgrow it by 2^8.
-    const bool grow0 = tmax[0] > m_ref[0] + kLazyRescale;
-    const bool grow1 = tmax[1] > m_ref[1] + kLazyRescale;
-    const bool rescale = __builtin_amdgcn_ballot_w64(grow0 || grow1) != 0;
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      const bool grow = rt == 0 ? grow0 : grow1;
-      const float nref = grow ? tmax[rt] : m_ref[rt];
-      alpha[rt] = (m_ref[rt] == -INFINITY) ? 0.f : fast_exp2(m_ref[rt] - nref);
-      m_ref[rt] = nref;
-      const float ref = (nref == -INFINITY) ? 0.f : nref;
-      float psum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        float p[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          p[i] = fast_exp2(fmaf(sacc[kt][rt][i], scale_log2, -ref));
-          psum += p[i];
-        }
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const uint4 w = make_uint4(pack_bf16x2(p[8 * half + 0], p[8 * half + 1]),
-                                     pack_bf16x2(p[8 * half + 2], p[8 * half + 3]),
-                                     pack_bf16x2(p[8 * half + 4], p[8 * half + 5]),
-                                     pack_bf16x2(p[8 * half + 6], p[8 * half + 7]));
-          pb[rt][2 * kt + half] = __builtin_bit_cast(bf16x8_t, w);
-        }
-      }
-      l_run[rt] = l_run[rt] * alpha[rt] + psum;
-    }
-
-    // ---- O^T += V^T P^T: 4 dim tiles x 2 row tiles, one k-step per block ----
-    // (the rescale of O^T, when a row max moved, is folded in one 16-value
-    // accumulator at a time)
+  };
+  // O^T_r += V^T P^T_r for one step: one k-step per block, 4 accumulator chains.
+  auto pv = [&](int r, int step, const bf16x8_t (&pr)[4]) {
+    const int buf = step % kBufs;
 #pragma unroll
     for (int kb = 0; kb < kStepBlocks; ++kb) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         const bf16x8_t a =
             *reinterpret_cast<const bf16x8_t*>(&lds[buf][1][kb][dt * 32 * 32 + v_read]);
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          if (kb == 0 && rescale) oacc[dt][rt] *= alpha[rt];
-          oacc[dt][rt] = mfma32(a, pb[rt][kb], oacc[dt][rt]);
-        }
+        oacc[dt][r] = mfma32(a, pr[kb], oacc[dt][r]);
       }
     }
+  };
+  // Softmax of stream r at one step: P (bf16, 8 consecutive keys of each
+  // block), the row-sum update, and the rescale factor for O if the row's
+  // reference max moved.
+  // Causal / length / real-block mask of stream r's scores at one step, in
+  // place; run only on the steps that need it.
+  auto mask_scores = [&](int r, int step, int bits, f32x16_t (&sr)[2]) {
+    const int kbase = step * kKeys;
+    const int qpos = wave_pos0 + r * 32 + lm;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int kpos = kbase + kt * 32 + (i / 8) * 16 + lh * 8 + (i % 8);
+        const int blk_ok = (bits >> (2 * kt + i / 8)) & 1;
+        const int keep = (kpos <= qpos) & (kpos < L) & blk_ok;
+        sr[kt][i] = keep ? sr[kt][i] : -INFINITY;
+      }
+  };
+  auto sm = [&](int r, const f32x16_t (&x)[2], bf16x8_t (&pr)[4], float& alpha, bool& rescale) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, x[kt][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float tmax = mx * scale_log2;
+    // Move the row's reference max only when its scores outgrow it by 2^8.
+    const bool grow = tmax > m_ref[r] + kLazyRescale;
+    rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+    const float nref = grow ? tmax : m_ref[r];
+    alpha = (m_ref[r] == -INFINITY) ? 0.f : fast_exp2(m_ref[r] - nref);
+    m_ref[r] = nref;
+    const float ref = (nref == -INFINITY) ? 0.f : nref;
+    float psum = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      float p[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p[i] = fast_exp2(fmaf(x[kt][i], scale_log2, -ref));
+        psum += p[i];
+      }
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const uint4 w = make_uint4(pack_bf16x2(p[8 * half + 0], p[8 * half + 1]),
+                                   pack_bf16x2(p[8 * half + 2], p[8 * half + 3]),
+                                   pack_bf16x2(p[8 * half + 4], p[8 * half + 5]),
+                                   pack_bf16x2(p[8 * half + 6], p[8 * half + 7]));
+        pr[2 * kt + half] = __builtin_bit_cast(bf16x8_t, w);
+      }
+    }
+    l_run[r] = l_run[r] * alpha + psum;
+  };
+  // The step needs the mask if a key can lie past a row of the stream or the
+  // end, or a block of the step was not loaded.
+  auto needs_mask = [&](int r, int step, int bits) {
+    return (step * kKeys + kKeys - 1 > wave_pos0 + r * 32) || !step_clean(step, bits);
+  };
 
-    if (step + 1 < nsteps) store_step(buf ^ 1, step + 1);
+  f32x16_t sc[2][2];      // sc[r]: scores of stream r waiting for its softmax
+  bf16x8_t pp[2][4];      // pp[r]: P of stream r waiting for its p.v
+  float al[2] = {1.f, 1.f};
+  bool rs[2] = {false, false};
+
+  // One phase: the MFMA work of stream `mr` (p.v of step i, then q.k of step
+  // i + 1 when there is one) interleaved with the softmax of stream `vr` at
+  // step `vs`. The two are independent, so the matrix cores and the vector
+  // ALU run side by side. O of stream mr is rescaled first if its last
+  // softmax moved the reference max; the scores of stream vr are masked first
+  // on the steps that need it.
+  auto run_phase = [&](auto next_tag, int mr, int i, int vr, int vs, int vbits) {
+    constexpr bool kNext = decltype(next_tag)::value;
+    if (rs[mr]) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) scale_acc(oacc[dt][mr], al[mr]);
+      rs[mr] = false;
+    }
+    if (needs_mask(vr, vs, vbits)) mask_scores(vr, vs, vbits, sc[vr]);
+    pv(mr, i, pp[mr]);
+    if constexpr (kNext) qk(mr, i + 1, sc[mr]);
+    sm(vr, sc[vr], pp[vr], al[vr], rs[vr]);
+    // keep the softmax in this phase (the compiler would otherwise sink it
+    // next to its first use, away from the matrix work it should overlap)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) asm volatile("" ::"v"(pp[vr][k]));
+  };
+
+  // bits0, bits1, bits2: real-block masks of steps i, i + 1, i + 2
+  int bits0 = 0, bits1 = 0, bits2 = 0;
+  if (nsteps > 0) bits0 = load_step(0);
+  if (nsteps > 1) bits1 = load_step(1);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (nsteps > 0 && !step_clean(0, bits0)) patch_step(0, bits0);
+  if (nsteps > 1 && !step_clean(1, bits1)) patch_step(1, bits1);
+  __syncthreads();
+  if (nsteps > 0) {
+    qk(0, 0, sc[0]);
+    qk(1, 0, sc[1]);
+    if (needs_mask(0, 0, bits0)) mask_scores(0, 0, bits0, sc[0]);
+    sm(0, sc[0], pp[0], al[0], rs[0]);
+  }
+  for (int i = 0; i + 1 < nsteps; ++i) {
+    // step i + 1 landed before the last barrier; its V is patched here and
+    // first read after the next barrier
+    if (i >= 1 && !step_clean(i + 1, bits1)) patch_step(i + 1, bits1);
+    if (i + 2 < nsteps) bits2 = load_step(i + 2);
+    run_phase(std::true_type{}, 0, i, 1, i, bits0);
+    run_phase(std::true_type{}, 1, i, 0, i + 1, bits1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    bits0 = bits1;
+    bits1 = bits2;
+  }
+  if (nsteps > 0) {
+    // last step: p.v of both streams, the softmax of stream 1 in between
+    const int i = nsteps - 1;
+    run_phase(std::false_type{}, 0, i, 1, i, bits0);
+    if (rs[1]) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) scale_acc(oacc[dt][1], al[1]);
+    }
+    pv(1, i, pp[1]);
   }
 
   // ---- normalise and write O (this lane: row lm of each row tile) ----
