@@ -3,15 +3,14 @@
 // chunking splits the same work; Section 1: max_num_batched_tokens bounds
 // the chunk).
 //
-// Work tile = (kv head g, 64 * 4 / G consecutive new rows of one sequence).
-// A workgroup of 4 wavefronts owns one tile: wave w serves query head
-// g * G + w % G over 64 rows (two row tiles of 32). K/V steps of 64 keys (4
-// blocks) are gathered through the block table into double-buffered LDS once
-// per workgroup and shared by the G query heads of the group.
+// Work tile = (kv head g, 32 * 8 / G consecutive new rows of one sequence).
+// A workgroup of 8 wavefronts (two per SIMD) owns one tile: wave w serves
+// query head g * G + w % G over 32 rows. K/V steps of 64 keys (4 blocks) are
+// gathered through the block table straight into LDS (global_load_lds) once
+// per workgroup and shared by the G query heads of the group; four LDS
+// buffers let the gather run two steps ahead with one barrier per step.
 //
-// Per wave and step, with v_mfma_f32_32x32x16_bf16 (four independent
-// accumulator chains are enough to keep it busy, where the 16x16x32 form
-// needs sixteen):
+// Per wave and step, with v_mfma_f32_32x32x16_bf16:
 //   S^T[key][row] = K[key][:] . Q[row][:]   A = K rows read from the
 //       chunk-major K tile, B = Q^T held in registers for the whole kernel.
 //       The A rows of a 32-key tile are loaded in a permuted key order so
@@ -25,6 +24,9 @@
 //   O^T[d][row] += V^T[d][key] P^T[key][row]   A = 16-byte runs of the
 //       dim-major V tile, B = the bf16 P values of 8 consecutive keys of one
 //       block, already in the lane that produced them.
+// Software pipeline: while a wave computes the softmax of step i on the
+// vector ALU, its matrix work is p.v of step i - 1 and q.k of step i + 1, so
+// both units stay busy; the second wave of the SIMD covers the LDS latency.
 // V rows are stored in LDS with their two 16-byte halves swapped on every
 // other group of 8 rows, so the A reads of 16 rows hit 16 distinct bank
 // groups. The causal mask (bottom-right: row i at position L - n + i sees
@@ -46,7 +48,10 @@ constexpr int kKeys = 64;                  // keys per step
 constexpr int kStepBlocks = 4;             // blocks per step
 constexpr int kTileBytes = kBS * kD * 2;   // one (block, K/V, head) tile: 4 KiB
 constexpr float kLazyRescale = 8.f;        // log2 headroom before the max moves
-constexpr int kBufs = 3;                   // LDS steps in the software pipeline
+constexpr int kKBufs = 3;                  // LDS K steps (gathered three steps ahead)
+constexpr int kVBufs = 3;                  // LDS V steps (gathered one step ahead)
+constexpr int kWaves = 8;                  // wavefronts per workgroup
+constexpr int kThreads = kWaves * kWave;
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
@@ -54,23 +59,42 @@ __device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// acc *= a on an accumulator that lives in AGPRs. The running output stays in
-// the accumulator registers the matrix instructions write; a plain vector
-// multiply would make the compiler carry it in VGPRs and copy it across on
-// every step, although the rescale itself is rare.
-__device__ __forceinline__ void scale_acc(f32x16_t& acc, float a) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    float x = acc[i];
-    float t;
-    asm volatile(
-        "v_accvgpr_read_b32 %1, %0\n\t"
-        "v_mul_f32 %1, %1, %2\n\t"
-        "v_accvgpr_write_b32 %0, %1"
-        : "+a"(x), "=&v"(t)
-        : "v"(a));
-    acc[i] = x;
-  }
+// max(a, b, c) in one instruction. The scores here are never NaN (masked
+// keys are set to -inf by a select), so the IEEE NaN handling that fmaxf
+// adds around every operand is not needed.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+constexpr uint32_t kBf16OnePair = 0x3f803f80u;   // (1.0, 1.0) in bf16
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes go
+// to LDS byte address lds + 16 l (lds must be wave-uniform). Issued as inline
+// assembly so that the compiler does not treat it as an LDS store that every
+// later LDS read must wait for: the callers wait for these loads themselves
+// (s_waitcnt vmcnt) before the barrier that publishes the data.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gptr), "s"(lds)
+      : "memory", "m0");
+}
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// The lane's index in its wavefront, computed afresh at each call (volatile,
+// so it is not merged with an earlier copy that would have to stay live).
+__device__ __forceinline__ int lane_id_fresh() {
+  int r;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(r));
+  return r;
 }
 
 }  // namespace
@@ -113,14 +137,15 @@ __global__ __launch_bounds__(256) void prefill_tile_map_kernel(const int* __rest
 }
 
 template <int G>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+                          amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ kv,
                     int num_blocks, const int* __restrict__ block_table,
                     const int* __restrict__ seq_lens, const int* __restrict__ cu,
                     uint16_t* __restrict__ out, const int2* __restrict__ tiles,
                     const int* __restrict__ tile_count, int num_q_heads, int num_kv_heads,
                     int max_blocks, int max_seq_len, float scale_log2) {
-  constexpr int kRows = 64 * 4 / G;      // rows per work tile
+  constexpr int kRows = 32 * kWaves / G;   // rows per work tile
   const int wid = blockIdx.x;
   const int g = wid % num_kv_heads;
   const int ti = wid / num_kv_heads;
@@ -132,17 +157,20 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform per wavefront
   const int lane = tid % kWave;
   const int h = g * G + wave % G;
-  const int row0 = q0 + (wave / G) * 64;        // first row of this wave
+  const int row0 = q0 + (wave / G) * 32;        // first row of this wave
   const int cu0 = cu[s];
   const int n = cu[s + 1] - cu0;
   int L = seq_lens[s];
-  L = min(max(L, 0), min(max_seq_len, max_blocks * kBS));
+  L = __builtin_amdgcn_readfirstlane(min(max(L, 0), min(max_seq_len, max_blocks * kBS)));
   const int c = L - n;                          // cached context before the chunk
   const int wg_rows = min(kRows, n - q0);
   const int last_pos = min(c + q0 + wg_rows - 1, L - 1);
-  const int nsteps = last_pos >= 0 ? last_pos / kKeys + 1 : 0;
+  const int N = last_pos >= 0 ? last_pos / kKeys + 1 : 0;   // steps of the tile
 
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kBufs][2][kStepBlocks][kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_k[kKBufs][kStepBlocks][kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_v[kVBufs][kStepBlocks][kTileBytes];
+  // Q^T operand of each wave: [wave][k-step][lane] 16-byte runs.
+  __shared__ __attribute__((aligned(16))) uint8_t lds_q[kWaves][8][kWave * 16];
 
   const size_t block_bytes = 2 * (size_t)num_kv_heads * kTileBytes;
   const size_t k_off = (size_t)g * kTileBytes;
@@ -159,69 +187,83 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int k_blk = ka / 2;                              // block within the key tile
   const int k_slot = 8 * kb4 + 4 * (ka % 2) + ke;        // slot within the block
 
-  // ---- Q^T operands of the wave's two streams of 32 rows ----
-  bf16x8_t qb[2][8];
+  // ---- Q^T operand of the wave's 32 rows, gathered into LDS ----
+  // Lane (lm, lh) of k-step ks holds dims ks * 16 + lh * 8 .. + 8 of row
+  // row0 + lm; rows past the chunk read the chunk's last row (never written).
+  {
+    const int row = min(row0 + lm, n - 1);
+    const uint16_t* qrow = q + (size_t)(cu0 + row) * qstride + (size_t)h * kD + lh * 8;
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int row = row0 + r * 32 + lm;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row < n)
-        v = *reinterpret_cast<const uint4*>(q + (size_t)(cu0 + row) * qstride +
-                                           (size_t)h * kD + ks * 16 + lh * 8);
-      qb[r][ks] = __builtin_bit_cast(bf16x8_t, v);
-    }
+    for (int ks = 0; ks < 8; ++ks)
+      dma16(qrow + ks * 16, __builtin_amdgcn_readfirstlane(lds_addr(&lds_q[wave][ks][0])));
   }
 
-  f32x16_t oacc[4][2];
+  f32x16_t oacc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int r = 0; r < 2; ++r)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[dt][r][i] = 0.f;
-  float m_ref[2] = {-INFINITY, -INFINITY};   // reference max of each row (log2 domain)
-  float l_run[2] = {0.f, 0.f};               // lane-partial row sums
+    for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
+  float m_ref = -INFINITY;   // reference max of the lane's row (log2 domain)
+  float l_run = 0.f;         // lane-partial row sum
 
-  // ---- gather of one 64-key step straight into LDS (global_load_lds, 16 B/lane) ----
-  // Each wavefront fills a contiguous 1 KiB quarter of every 4 KiB tile. K is
-  // copied as stored; for V the lane picks the global 16 bytes that belong at
-  // its swizzled LDS position (row tid / 2, half tid % 2 holds global half
-  // (tid % 2) ^ ((row >> 3) & 1)). A block past L or with an id outside
-  // [0, num_blocks) is replaced by block 0 (the host guarantees one exists);
-  // the returned bit mask (bit kb: block kb is real) lets the softmax mask its
-  // keys and patch_step zero its values.
-  const int vrow = tid / 2;
-  const int v_src = vrow * 32 + (((tid % 2) ^ ((vrow >> 3) & 1)) * 16);
-  auto load_step = [&](int step) {
-    const int buf = step % kBufs;
+  // ---- gather of K or V of one 64-key step straight into LDS (global_load_lds) ----
+  // A half step is 4 tiles of 4 KiB (blocks 0..3); in round j wavefront w
+  // fills quarter (w + 8 j) % 4 of tile (w + 8 j) / 4, a contiguous 1 KiB with
+  // 16 bytes per lane. K is copied as stored; for V the lane picks the global
+  // 16 bytes that belong at its swizzled LDS position (row pos / 2, half
+  // pos % 2 holds global half (pos % 2) ^ ((row >> 3) & 1)). A block past L
+  // or with an id outside [0, num_blocks) is replaced by block 0 (the host
+  // guarantees one exists); the returned bit mask (bit kb: block kb is real)
+  // lets the softmax mask its keys and patch_v zero its values.
+  auto load_half = [&](auto v_tag, int step) __attribute__((always_inline)) {
+    constexpr bool kV = decltype(v_tag)::value;
     const int kbase = step * kKeys;
+    // block id of block kb of the step, or -1 if it is not real
+    auto block_id = [&](int kb) __attribute__((always_inline)) {
+      const int key0 = kbase + kb * kBS;
+      const int id = key0 < L ? bt[key0 / kBS] : -1;
+      return (unsigned)id < (unsigned)num_blocks ? id : -1;
+    };
     int bits = 0;
 #pragma unroll
-    for (int kb = 0; kb < kStepBlocks; ++kb) {
-      const int key0 = kbase + kb * kBS;
-      int id = key0 < L ? bt[key0 / kBS] : -1;
-      const bool ok = (unsigned)id < (unsigned)num_blocks;
-      bits |= ok ? (1 << kb) : 0;
-      const uint8_t* base = kv + (size_t)(ok ? id : 0) * block_bytes;
-      __builtin_amdgcn_global_load_lds(base + k_off + tid * 16, &lds[buf][0][kb][wave * 1024], 16,
-                                       0, 0);
-      __builtin_amdgcn_global_load_lds(base + v_off + v_src, &lds[buf][1][kb][wave * 1024], 16,
-                                       0, 0);
+    for (int kb = 0; kb < kStepBlocks; ++kb) bits |= block_id(kb) >= 0 ? (1 << kb) : 0;
+    // The lane id is recomputed here rather than kept live across the step.
+    const int ln = lane_id_fresh();
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int kb = (wave + kWaves * j) / 4;     // wave-uniform
+      const int quarter = (wave + kWaves * j) % 4;
+      const int id = block_id(kb);
+      const uint8_t* base = kv + (size_t)(id >= 0 ? id : 0) * block_bytes + (kV ? v_off : k_off);
+      const int pos = quarter * kWave + ln;       // 16-byte position in the tile
+      if constexpr (kV) {
+        const int vrow = pos / 2;
+        const int src = vrow * 32 + (((pos % 2) ^ ((vrow >> 3) & 1)) * 16);
+        dma16(base + src, __builtin_amdgcn_readfirstlane(
+                              lds_addr(&lds_v[step % kVBufs][kb][quarter * 1024])));
+      } else {
+        dma16(base + pos * 16, __builtin_amdgcn_readfirstlane(
+                                   lds_addr(&lds_k[step % kKBufs][kb][quarter * 1024])));
+      }
     }
     return bits;
   };
   // Zero the V slots of a landed step that must not contribute: blocks that
   // are not real, and slots at or past L (their bytes may be NaN, and a zero
-  // weight times NaN is NaN). Called only when such slots exist.
-  auto patch_step = [&](int step, int bits) {
-    const int buf = step % kBufs;
+  // weight times NaN is NaN). Every wavefront patches the whole step right
+  // before its own p.v reads it: the writes of different wavefronts are
+  // identical and idempotent, so no barrier is needed between them. Called
+  // only when such slots exist.
+  auto patch_v = [&](int step, int bits) __attribute__((always_inline)) {
     const int kbase = step * kKeys;
-    const int half_g = (tid % 2) ^ ((vrow >> 3) & 1);
 #pragma unroll
-    for (int kb = 0; kb < kStepBlocks; ++kb) {
-      uint4* v = reinterpret_cast<uint4*>(&lds[buf][1][kb][tid * 16]);
+    for (int j = 0; j < 16; ++j) {
+      const int cidx = lane + kWave * j;          // 16-byte chunk of the 4 V tiles
+      const int kb = cidx / 256;
+      const int pos = cidx % 256;
+      const int vrow = pos / 2;
+      const int half_g = (pos % 2) ^ ((vrow >> 3) & 1);
+      uint4* v = reinterpret_cast<uint4*>(&lds_v[step % kVBufs][kb][pos * 16]);
       if (!((bits >> kb) & 1)) {
         *v = make_uint4(0, 0, 0, 0);
         continue;
@@ -239,52 +281,48 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       *v = make_uint4(w[0], w[1], w[2], w[3]);
     }
   };
-  auto step_clean = [&](int step, int bits) { return bits == 0xf && (step + 1) * kKeys <= L; };
-  // All of this wave's direct-to-LDS loads have landed.
-  auto wait_loads = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+  auto step_clean = [&](int step, int bits) __attribute__((always_inline)) { return bits == 0xf && (step + 1) * kKeys <= L; };
 
   const int wave_pos0 = c + row0;   // position of the wave's first row
   const int v_read = lm * 32 + ((lh ^ ((lm >> 3) & 1)) * 16);
 
-  // S^T of stream r for one step: 2 key tiles x 8 k-steps of 16 dims.
-  auto qk = [&](int r, int step, f32x16_t (&sa)[2]) {
-    const int buf = step % kBufs;
+  // S^T for one step: 2 key tiles x 8 k-steps of 16 dims.
+  auto qk = [&](int step, f32x16_t (&sa)[2]) {
+    const int buf = step % kKBufs;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sa[kt][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
+      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(&lds_q[wave][ks][lane * 16]);
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const int chunk = 2 * ks + lh;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
-            &lds[buf][0][2 * kt + k_blk][(chunk * kBS + k_slot) * 16]);
-        sa[kt] = mfma32(a, qb[r][ks], sa[kt]);
+            &lds_k[buf][2 * kt + k_blk][(chunk * kBS + k_slot) * 16]);
+        sa[kt] = mfma32(a, b, sa[kt]);
       }
     }
   };
-  // O^T_r += V^T P^T_r for one step: one k-step per block, 4 accumulator chains.
-  auto pv = [&](int r, int step, const bf16x8_t (&pr)[4]) {
-    const int buf = step % kBufs;
+  // O^T += V^T P^T for one step: one k-step per block, 4 accumulator chains.
+  auto pv = [&](int step, const bf16x8_t (&pr)[4]) {
+    const int buf = step % kVBufs;
 #pragma unroll
     for (int kb = 0; kb < kStepBlocks; ++kb) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(&lds[buf][1][kb][dt * 32 * 32 + v_read]);
-        oacc[dt][r] = mfma32(a, pr[kb], oacc[dt][r]);
+            *reinterpret_cast<const bf16x8_t*>(&lds_v[buf][kb][dt * 32 * 32 + v_read]);
+        oacc[dt] = mfma32(a, pr[kb], oacc[dt]);
       }
     }
   };
-  // Softmax of stream r at one step: P (bf16, 8 consecutive keys of each
-  // block), the row-sum update, and the rescale factor for O if the row's
-  // reference max moved.
-  // Causal / length / real-block mask of stream r's scores at one step, in
-  // place; run only on the steps that need it.
-  auto mask_scores = [&](int r, int step, int bits, f32x16_t (&sr)[2]) {
+  // Causal / length / real-block mask of one step's scores, in place; run
+  // only on the steps that need it.
+  auto mask_scores = [&](int step, int bits, f32x16_t (&sr)[2]) {
     const int kbase = step * kKeys;
-    const int qpos = wave_pos0 + r * 32 + lm;
+    const int qpos = wave_pos0 + lm;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -295,7 +333,13 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
         sr[kt][i] = keep ? sr[kt][i] : -INFINITY;
       }
   };
-  auto sm = [&](int r, const f32x16_t (&x)[2], bf16x8_t (&pr)[4], float& alpha, bool& rescale) {
+  auto needs_mask = [&](int step, int bits) __attribute__((always_inline)) {
+    return (step * kKeys + kKeys - 1 > wave_pos0) || !step_clean(step, bits);
+  };
+  // Softmax of one step: P (bf16, 8 consecutive keys of each block), the
+  // row-sum update, and the rescale factor for O if the row's reference max
+  // moved.
+  auto sm = [&](const f32x16_t (&x)[2], bf16x8_t (&pr)[4], float& alpha, bool& rescale) {
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -304,11 +348,11 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
     const float tmax = mx * scale_log2;
     // Move the row's reference max only when its scores outgrow it by 2^8.
-    const bool grow = tmax > m_ref[r] + kLazyRescale;
+    const bool grow = tmax > m_ref + kLazyRescale;
     rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
-    const float nref = grow ? tmax : m_ref[r];
-    alpha = (m_ref[r] == -INFINITY) ? 0.f : fast_exp2(m_ref[r] - nref);
-    m_ref[r] = nref;
+    const float nref = grow ? tmax : m_ref;
+    alpha = (m_ref == -INFINITY) ? 0.f : fast_exp2(m_ref - nref);
+    m_ref = nref;
     const float ref = (nref == -INFINITY) ? 0.f : nref;
     float psum = 0.f;
 #pragma unroll
@@ -328,93 +372,186 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
         pr[2 * kt + half] = __builtin_bit_cast(bf16x8_t, w);
       }
     }
-    l_run[r] = l_run[r] * alpha + psum;
-  };
-  // The step needs the mask if a key can lie past a row of the stream or the
-  // end, or a block of the step was not loaded.
-  auto needs_mask = [&](int r, int step, int bits) {
-    return (step * kKeys + kKeys - 1 > wave_pos0 + r * 32) || !step_clean(step, bits);
+    l_run = l_run * alpha + psum;
   };
 
-  f32x16_t sc[2][2];      // sc[r]: scores of stream r waiting for its softmax
-  bf16x8_t pp[2][4];      // pp[r]: P of stream r waiting for its p.v
-  float al[2] = {1.f, 1.f};
-  bool rs[2] = {false, false};
+  // bitsm1, bits0 .. bits3: real-block masks of steps i - 1, i .. i + 3
+  int bitsm1 = 0, bits0 = 0, bits1 = 0, bits2 = 0, bits3 = 0;
+  f32x16_t sA[2], sB[2];    // scores of even / odd steps
+  bf16x8_t pA[4], pB[4];    // P of even / odd steps
 
-  // One phase: the MFMA work of stream `mr` (p.v of step i, then q.k of step
-  // i + 1 when there is one) interleaved with the softmax of stream `vr` at
-  // step `vs`. The two are independent, so the matrix cores and the vector
-  // ALU run side by side. O of stream mr is rescaled first if its last
-  // softmax moved the reference max; the scores of stream vr are masked first
-  // on the steps that need it.
-  auto run_phase = [&](auto next_tag, int mr, int i, int vr, int vs, int vbits) {
-    constexpr bool kNext = decltype(next_tag)::value;
-    if (rs[mr]) {
+  // One pipeline step i: gather K of step i + 3 and V of step i + 1, then the
+  // matrix work (p.v of step i - 1, q.k of step i + 1) next to the softmax of
+  // step i. The step ends by waiting for the gathers of the earlier steps
+  // only (those of this step get the whole next step to land) and a barrier;
+  // then O takes the rescale of step i's softmax, between the p.v of steps
+  // i - 1 and i.
+  //
+  // The matrix and softmax work is laid out by hand in 32 issue slots: slot
+  // k issues matrix instruction k (p.v for k < 16, q.k after), the LDS read
+  // of the operand four slots ahead, and a fixed share of the softmax
+  // (slots 0-7: row max, slot 8: reference max and rescale factor, slots
+  // 9-31: exponentials, row sum, bf16 packing). A wavefront issues in order,
+  // so without this the vector work would queue behind runs of matrix
+  // instructions instead of running beside them.
+  auto phase = [&](auto qk_tag, auto pv_tag, int i, f32x16_t (&s_cur)[2],
+                   f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4], bf16x8_t (&p_cur)[4]) __attribute__((always_inline)) {
+    constexpr bool kQK = decltype(qk_tag)::value;
+    constexpr bool kPV = decltype(pv_tag)::value;
+    if (i + 3 < N) bits3 = load_half(std::false_type{}, i + 3);
+    if (i + 1 < N) load_half(std::true_type{}, i + 1);
+    if (kPV && !step_clean(i - 1, bitsm1)) patch_v(i - 1, bitsm1);
+    if (needs_mask(i, bits0)) mask_scores(i, bits0, s_cur);
+
+    const int vbuf = (i + kVBufs - 1) % kVBufs;   // V of step i - 1
+    const int kbuf = (i + 1) % kKBufs;            // K of step i + 1
+    auto has_mfma = [&](int k) __attribute__((always_inline)) { return k < 16 ? kPV : kQK; };
+    auto a_frag = [&](int k) __attribute__((always_inline)) {
+      if (k < 16)
+        return *reinterpret_cast<const bf16x8_t*>(
+            &lds_v[vbuf][k / 4][(k % 4) * 32 * 32 + v_read]);
+      const int ks = (k - 16) / 2, kt = (k - 16) % 2;
+      return *reinterpret_cast<const bf16x8_t*>(
+          &lds_k[kbuf][2 * kt + k_blk][((2 * ks + lh) * kBS + k_slot) * 16]);
+    };
+    auto q_frag = [&](int ks) __attribute__((always_inline)) {
+      return *reinterpret_cast<const bf16x8_t*>(&lds_q[wave][ks][lane * 16]);
+    };
+    constexpr int kAhead = 4;
+    bf16x8_t fr[kAhead + 1];
+    bf16x8_t qf[3];
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) scale_acc(oacc[dt][mr], al[mr]);
-      rs[mr] = false;
+    for (int k = 0; k < kAhead; ++k) {
+      if (has_mfma(k)) fr[k % (kAhead + 1)] = a_frag(k);
+      if (kQK && k >= 16 && (k - 16) % 2 == 0) qf[((k - 16) / 2) % 3] = q_frag((k - 16) / 2);
     }
-    if (needs_mask(vr, vs, vbits)) mask_scores(vr, vs, vbits, sc[vr]);
-    pv(mr, i, pp[mr]);
-    if constexpr (kNext) qk(mr, i + 1, sc[mr]);
-    sm(vr, sc[vr], pp[vr], al[vr], rs[vr]);
-    // keep the softmax in this phase (the compiler would otherwise sink it
+    float mp0 = -INFINITY, mp1 = -INFINITY, ref = 0.f, alpha = 1.f, psum = 0.f;
+    bool rescale = false;
+    float pe[32];
+    uint32_t pw[16];
+    f32x16_t zero;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) zero[e] = 0.f;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+      // operand reads for slot k + kAhead
+      const int kn = k + kAhead;
+      if (kn < 32 && has_mfma(kn)) fr[kn % (kAhead + 1)] = a_frag(kn);
+      if (kQK && kn < 32 && kn >= 16 && (kn - 16) % 2 == 0)
+        qf[((kn - 16) / 2) % 3] = q_frag((kn - 16) / 2);
+      // matrix instruction k
+      if (k < 16) {
+        if (kPV) oacc[k % 4] = mfma32(fr[k % (kAhead + 1)], p_prev[k / 4], oacc[k % 4]);
+      } else if (kQK) {
+        const int ks = (k - 16) / 2, kt = (k - 16) % 2;
+        s_nxt[kt] = mfma32(fr[k % (kAhead + 1)], qf[ks % 3], ks == 0 ? zero : s_nxt[kt]);
+      }
+      // softmax share of slot k
+      if (k < 8) {
+        const int e = 4 * k;
+        mp0 = max3f(mp0, s_cur[e / 16][e % 16], s_cur[e / 16][e % 16 + 1]);
+        mp1 = max3f(mp1, s_cur[e / 16][e % 16 + 2], s_cur[e / 16][e % 16 + 3]);
+      } else if (k == 8) {
+        float mx = max3f(mp0, mp1, mp1);
+        mx = max3f(mx, __shfl_xor(mx, 32, kWave), mx);
+        const float tmax = mx * scale_log2;
+        // Move the row's reference max only when its scores outgrow it by 2^8.
+        const bool grow = tmax > m_ref + kLazyRescale;
+        rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+        const float nref = grow ? tmax : m_ref;
+        alpha = (m_ref == -INFINITY) ? 0.f : fast_exp2(m_ref - nref);
+        m_ref = nref;
+        ref = (nref == -INFINITY) ? 0.f : nref;
+      } else {
+        const int e0 = ((k - 9) * 32) / 23, e1 = ((k - 8) * 32) / 23;
+#pragma unroll
+        for (int e = e0; e < e1; ++e) {
+          pe[e] = fast_exp2(fmaf(s_cur[e / 16][e % 16], scale_log2, -ref));
+          if (e % 2 == 1) {
+            // the row sum adds the bf16 values that p.v multiplies
+            pw[e / 2] = pack_bf16x2(pe[e - 1], pe[e]);
+            psum = dot2_bf16(pw[e / 2], kBf16OnePair, psum);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      p_cur[kb] = __builtin_bit_cast(
+          bf16x8_t, make_uint4(pw[4 * kb], pw[4 * kb + 1], pw[4 * kb + 2], pw[4 * kb + 3]));
+    l_run = l_run * alpha + psum;
+    // keep the softmax in its slots (the compiler would otherwise sink it
     // next to its first use, away from the matrix work it should overlap)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) asm volatile("" ::"v"(pp[vr][k]));
-  };
-
-  // bits0, bits1, bits2: real-block masks of steps i, i + 1, i + 2
-  int bits0 = 0, bits1 = 0, bits2 = 0;
-  if (nsteps > 0) bits0 = load_step(0);
-  if (nsteps > 1) bits1 = load_step(1);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (nsteps > 0 && !step_clean(0, bits0)) patch_step(0, bits0);
-  if (nsteps > 1 && !step_clean(1, bits1)) patch_step(1, bits1);
-  __syncthreads();
-  if (nsteps > 0) {
-    qk(0, 0, sc[0]);
-    qk(1, 0, sc[1]);
-    if (needs_mask(0, 0, bits0)) mask_scores(0, 0, bits0, sc[0]);
-    sm(0, sc[0], pp[0], al[0], rs[0]);
-  }
-  for (int i = 0; i + 1 < nsteps; ++i) {
-    // step i + 1 landed before the last barrier; its V is patched here and
-    // first read after the next barrier
-    if (i >= 1 && !step_clean(i + 1, bits1)) patch_step(i + 1, bits1);
-    if (i + 2 < nsteps) bits2 = load_step(i + 2);
-    run_phase(std::true_type{}, 0, i, 1, i, bits0);
-    run_phase(std::true_type{}, 1, i, 0, i + 1, bits1);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    for (int k = 0; k < 4; ++k) asm volatile("" ::"v"(p_cur[k]));
+    asm volatile("" ::"v"(l_run));
+    // wait for the gathers of steps before this one (each thread issued two
+    // for K when i + 3 < N and two for V when i + 1 < N in this step)
+    if (i + 3 < N)
+      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else if (i + 1 < N)
+      asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (rescale) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) oacc[dt] *= alpha;
+    }
+    bitsm1 = bits0;
     bits0 = bits1;
     bits1 = bits2;
-  }
-  if (nsteps > 0) {
-    // last step: p.v of both streams, the softmax of stream 1 in between
-    const int i = nsteps - 1;
-    run_phase(std::false_type{}, 0, i, 1, i, bits0);
-    if (rs[1]) {
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) scale_acc(oacc[dt][1], al[1]);
+    bits2 = bits3;
+  };
+
+  if (N > 0) {
+    bits0 = load_half(std::false_type{}, 0);
+    if (N > 1) bits1 = load_half(std::false_type{}, 1);
+    if (N > 2) bits2 = load_half(std::false_type{}, 2);
+    load_half(std::true_type{}, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    qk(0, sA);
+    __syncthreads();   // K of step 0 is read; step 0 of the pipeline gathers step 3 into its buffer
+    constexpr std::true_type T{};
+    constexpr std::false_type F{};
+    if (N > 1)
+      phase(T, F, 0, sA, sB, pB, pA);
+    else
+      phase(F, F, 0, sA, sB, pB, pA);
+    int i = 1;
+    for (; i + 1 <= N - 2; i += 2) {
+      phase(T, T, i, sB, sA, pA, pB);
+      phase(T, T, i + 1, sA, sB, pB, pA);
     }
-    pv(1, i, pp[1]);
+    if (i <= N - 2) {
+      phase(T, T, i, sB, sA, pA, pB);
+      ++i;
+    }
+    // p.v of the last step (its V landed by the last step's full wait)
+    if (N > 1) {
+      if (i & 1)
+        phase(F, T, i, sB, sA, pA, pB);
+      else
+        phase(F, T, i, sA, sB, pB, pA);
+    }
+    if (!step_clean(N - 1, bitsm1)) patch_v(N - 1, bitsm1);
+    pv(N - 1, ((N - 1) & 1) ? pB : pA);
   }
 
-  // ---- normalise and write O (this lane: row lm of each row tile) ----
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    float lt = l_run[rt] + __shfl_xor(l_run[rt], 32, kWave);
+  // ---- normalise and write O (this lane: row lm) ----
+  {
+    const float lt = l_run + __shfl_xor(l_run, 32, kWave);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int r = row0 + rt * 32 + lm;
+    const int r = row0 + lm;
     if (r < n) {
       uint16_t* orow = out + (size_t)(cu0 + r) * qstride + (size_t)h * kD;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
-          const f32x16_t& o = oacc[dt][rt];
+          const f32x16_t& o = oacc[dt];
           const uint2 w = make_uint2(pack_bf16x2(o[4 * a + 0] * inv, o[4 * a + 1] * inv),
                                      pack_bf16x2(o[4 * a + 2] * inv, o[4 * a + 3] * inv));
           *reinterpret_cast<uint2*>(orow + dt * 32 + a * 8 + lh * 4) = w;
@@ -426,7 +563,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
 
 template <int G>
 static hipError_t launch_prefill_t(const PrefillArgs& a) {
-  constexpr int kRowsPerTile = 64 * 4 / G;
+  constexpr int kRowsPerTile = 32 * kWaves / G;
   int* count = reinterpret_cast<int*>(a.workspace);
   int2* tiles = reinterpret_cast<int2*>(static_cast<uint8_t*>(a.workspace) + 16);
   const int max_tiles =
@@ -443,7 +580,7 @@ static hipError_t launch_prefill_t(const PrefillArgs& a) {
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   trace_before(a.stream, "prefill");
-  hipLaunchKernelGGL((prefill_kernel<G>), dim3((unsigned)blocks), dim3(256), 0, a.stream,
+  hipLaunchKernelGGL((prefill_kernel<G>), dim3((unsigned)blocks), dim3(kThreads), 0, a.stream,
                      static_cast<const uint16_t*>(a.q), static_cast<const uint8_t*>(a.kv),
                      a.num_blocks, a.block_table, a.seq_lens, a.cu_seqlens_q,
                      static_cast<uint16_t*>(a.out), tiles, count, a.num_q_heads,
