@@ -39,7 +39,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
-                    choices=["all", "decode", "prefill", "mixed", "toggle", "elastic", "copy"],
+                    choices=["all", "decode", "prefill", "mixed", "append", "toggle", "elastic",
+                             "copy"],
                     help="'all' = headline decode plus the prefill, mixed-step and toggle "
                          "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
                          "scales the HBM byte counters")
@@ -225,6 +226,39 @@ def mixed_leg(args, K, work):
     return {"workload": spec.name, "ms_per_step": ms, "kernel_ms": means,
             "prefill_tflops": flops / (means["prefill"] * 1e-3) / 1e12,
             "decode_gbs": dbytes / (means["decode_split"] * 1e-3) / 1e9}
+
+
+def append_leg(args, K, work):
+    """Writing a step's new K/V rows into the paged layer of the decode
+    workload's size (40704 blocks, 2.5 GiB): a decode step (one token for each
+    of 256 sequences, distinct random slots) and an 8192-token prefill chunk of
+    one sequence (consecutive slots through 512 random blocks)."""
+    from workloads.append import make_append
+    nb = 40704
+    layer = torch.empty(nb * 2 * 8 * 16 * 128, dtype=torch.bfloat16, device="cuda")
+    res = {}
+    for name, T in (("decode_step256", 256), ("prefill_chunk8192", 8192)):
+        a = make_append(T, num_kv_heads=8, head_dim=128, dtype="bf16", num_blocks=nb,
+                        block_size=16, seed=4242 + T)
+        if T > 256:
+            # one sequence's chunk: consecutive slots through its (random) blocks
+            blocks = torch.randperm(nb, generator=torch.Generator().manual_seed(T))[:T // 16]
+            t = np.arange(T)
+            a.slot_mapping = (blocks.numpy()[t // 16].astype(np.int64) * 16 +
+                              t % 16).astype(np.int32)
+        k, v = a.k_new.cuda(), a.v_new.cuda()
+        sm = torch.from_numpy(a.slot_mapping).cuda()
+
+        def step():
+            K.kv_append(k, v, sm, layer, nb)
+
+        ms, kern_ms, _ = timed(step, args.steps, args.warmup, K, "kv_append")
+        nbytes = work.append_bytes(T, 8, 128, 2)
+        log(f"append {name}: {ms * 1e3:.1f} us/call, kernel {kern_ms * 1e3:.1f} us, "
+            f"{nbytes / kern_ms / 1e6:.0f} GB/s")
+        res[name] = {"us_per_call": ms * 1e3, "kernel_us": kern_ms * 1e3,
+                     "bytes_per_call": nbytes, "roofline": roofline_hbm(nbytes, kern_ms)}
+    return res
 
 
 def toggle_leg(K):
@@ -442,6 +476,13 @@ def main():
                         config={"workload": "prefill_chunk8192_ctx24576_bf16"})
     if args.workload in ("all", "mixed"):
         line["mixed_step"] = mixed_leg(args, K, work)
+    if args.workload in ("all", "append"):
+        line["kv_append"] = append_leg(args, K, work)
+        if line["value"] is None:
+            p = line["kv_append"]["prefill_chunk8192"]
+            line.update(value=round(p["roofline"]["achieved"], 1), unit="GB/s",
+                        ms_per_step=round(p["us_per_call"] / 1e3, 5), roofline=p["roofline"],
+                        config={"workload": "kv_append_8192x8x128_bf16"})
     if args.workload in ("all", "toggle"):
         line["elastic_toggle"] = toggle_leg(K)
     if args.workload in ("all", "elastic"):

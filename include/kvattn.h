@@ -148,6 +148,31 @@ int kvattn_prefill_chunk(const void* q, const void* kv_layer, int num_blocks,
                          void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Write the new K and V rows of a step into their paged slots, the step that
+ * precedes attention on every decode and prefill step (Section 3, "The
+ * contiguity constraint": attention reads one tensor per layer indexed by
+ * block id; Section 2: the cache is handed out to sequences in fixed-size
+ * blocks).
+ *
+ * k_new, v_new  device, [num_tokens][num_kv_heads][head_dim] of dtype, 16-B
+ *               aligned; head_dim * element size must be a multiple of 16
+ * slot_mapping  device int32 [num_tokens]: token t goes to slot
+ *               block_id * block_size + slot_in_block of kv_layer; negative
+ *               slots (padding) and slots >= num_blocks * block_size are
+ *               skipped. Slots must be distinct (a repeated slot is written
+ *               by an unspecified one of its tokens).
+ * kv_layer      device, one layer in the layout above, 16-B aligned; the K row
+ *               lands in the chunk-major K tile, the V row in the dim-major V
+ *               tile of the block, for every kv head
+ * Supported: bf16 and fp32, block_size 16, rows (head_dim x element size) of
+ * 64 to 512 bytes in steps of 64 (KV_ERR_UNSUPPORTED otherwise). Asynchronous on
+ * stream; allocates nothing; num_tokens == 0 is a no-op.
+ */
+int kvattn_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mapping,
+                     void* kv_layer, int num_blocks, int num_tokens, int num_kv_heads,
+                     int head_dim, int block_size, kv_dtype dtype, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* Elastic per-layer KV pool (Section 3, "Two handles, one virtual range").
  * Each layer owns one reserved virtual range of base + elastic bytes plus one
  * unmapped guard granule. A base physical handle backs [0, base) for the

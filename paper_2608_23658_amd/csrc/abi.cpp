@@ -286,3 +286,49 @@ extern "C" int kvattn_prefill_chunk(const void* q, const void* kv_layer, int num
     return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: kernel not built");
   return hip_status(e, "kvattn_prefill_chunk launch");
 }
+
+extern "C" int kvattn_kv_append(const void* k_new, const void* v_new,
+                                const int32_t* slot_mapping, void* kv_layer, int num_blocks,
+                                int num_tokens, int num_kv_heads, int head_dim, int block_size,
+                                kv_dtype dtype, void* stream) {
+  clear_error();
+  if (dtype != KV_F32 && dtype != KV_BF16)
+    return set_error(KV_ERR_INVALID, "kvattn_kv_append: unknown dtype %d", (int)dtype);
+  const int esz = dtype == KV_BF16 ? 2 : 4;
+  if (num_tokens < 0) return set_error(KV_ERR_INVALID, "kvattn_kv_append: num_tokens < 0");
+  if (num_kv_heads <= 0 || head_dim <= 0 || (head_dim * esz) % 16)
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_kv_append: %d kv heads of dim %d (a row must be whole 16-byte "
+                     "chunks)", num_kv_heads, head_dim);
+  if (head_dim * esz % 64 || head_dim * esz > 512)
+    return set_error(KV_ERR_UNSUPPORTED,
+                     "kvattn_kv_append: rows must be 64 to 512 bytes in steps of 64, not %d",
+                     head_dim * esz);
+  if (block_size != 16)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_kv_append: block_size %d not built",
+                     block_size);
+  if (num_blocks <= 0 || (long long)num_blocks * block_size > 0x7fffffffLL)
+    return set_error(KV_ERR_INVALID, "kvattn_kv_append: num_blocks %d", num_blocks);
+  if (num_tokens == 0) return KV_OK;
+  if (!k_new || !v_new || !slot_mapping || !kv_layer)
+    return set_error(KV_ERR_INVALID, "kvattn_kv_append: null pointer argument");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(kv_layer))
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_kv_append: k_new, v_new and kv_layer must be 16-byte aligned");
+  kvattn::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.slot_mapping = slot_mapping;
+  a.kv = kv_layer;
+  a.num_blocks = num_blocks;
+  a.num_tokens = num_tokens;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.esz = esz;
+  a.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = kvattn::launch_append(a);
+  if (e == hipErrorNotSupported)
+    return set_error(KV_ERR_UNSUPPORTED,
+                     "kvattn_kv_append: rows must be 64 to 512 bytes in steps of 64");
+  return hip_status(e, "kvattn_kv_append launch");
+}

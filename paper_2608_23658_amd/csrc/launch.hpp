@@ -39,12 +39,23 @@ struct PrefillArgs {
   hipStream_t stream;
 };
 
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  const int32_t* slot_mapping;
+  void* kv;
+  int num_blocks, num_tokens, num_kv_heads, head_dim;
+  int esz;   // bytes per element: 2 (bf16) or 4 (fp32)
+  hipStream_t stream;
+};
+
 // Tracing hooks around each kernel launch (no-ops unless a trace is installed).
 void trace_before(hipStream_t stream, const char* kernel);
 void trace_after(hipStream_t stream);
 
 hipError_t launch_decode(const DecodeArgs& a);
 hipError_t launch_prefill(const PrefillArgs& a);
+hipError_t launch_append(const AppendArgs& a);
 
 // Query rows per prefill work tile (per query head).
 constexpr int kPrefillRows = 64;

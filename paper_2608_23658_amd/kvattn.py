@@ -59,6 +59,7 @@ def lib() -> ctypes.CDLL:
     _c(L.kvattn_prefill_workspace_bytes, sz, i32, i32, i32, i32)
     _c(L.kvattn_prefill_chunk, i32, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
        i32, i32, i32, f32, i32, vp, sz, vp)
+    _c(L.kvattn_kv_append, i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp)
     _c(L.kvpool_granularity, i32, i32, ctypes.POINTER(ctypes.c_size_t))
     _c(L.kvpool_create, i32, i32, i32, sz, sz, ctypes.POINTER(vp))
     _c(L.kvpool_layer_ptr, i32, vp, i32, ctypes.POINTER(vp))
@@ -189,6 +190,23 @@ def prefill_chunk(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch
                                     _dtype_code(q.dtype), _ptr(ws), ws.numel(), _stream(stream))
     check(rc)
     return out
+
+
+def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, slot_mapping: torch.Tensor, kv_layer,
+              num_blocks: int, *, block_size: int = 16, stream=None) -> None:
+    """Write ``k_new``/``v_new`` [T, Hkv, d] into the layer's slots ``slot_mapping`` [T] int32."""
+    T, Hkv, d = k_new.shape
+    if v_new.shape != k_new.shape or v_new.dtype != k_new.dtype:
+        raise ValueError("k_new and v_new must have the same shape and dtype")
+    if slot_mapping.dtype != torch.int32 or tuple(slot_mapping.shape) != (T,):
+        raise ValueError("slot_mapping must be int32 [num_tokens]")
+    _require_cuda(k_new, v_new, slot_mapping)
+    if not (k_new.is_contiguous() and v_new.is_contiguous() and slot_mapping.is_contiguous()):
+        raise ValueError("k_new, v_new and slot_mapping must be contiguous")
+    rc = lib().kvattn_kv_append(_ptr(k_new), _ptr(v_new), _ptr(slot_mapping), _ptr(kv_layer),
+                                int(num_blocks), T, Hkv, d, int(block_size),
+                                _dtype_code(k_new.dtype), _stream(stream))
+    check(rc)
 
 
 class KernelTrace:

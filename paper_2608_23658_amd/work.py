@@ -41,3 +41,9 @@ def decode_bytes(seq_lens, num_q_heads: int, num_kv_heads: int, head_dim: int, e
 
 def decode_flops(seq_lens, num_q_heads: int, head_dim: int) -> int:
     return 4 * head_dim * num_q_heads * int(np.asarray(seq_lens, dtype=np.int64).sum())
+
+
+def append_bytes(num_tokens: int, num_kv_heads: int, head_dim: int, esz: int) -> int:
+    """Writing T new rows: K and V read once and written once, plus the slots."""
+    row = num_kv_heads * head_dim * esz
+    return 4 * num_tokens * row + 4 * num_tokens

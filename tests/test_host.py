@@ -91,6 +91,37 @@ def test_prefill_argument_checks(L, kw, code):
     assert _prefill(L, **kw) == code
 
 
+def _append(L, **kw):
+    a = dict(k=A, v=A, sm=A, kv=A, nb=100, T=64, hkv=8, d=128, bs=16, dt=K.KV_BF16,
+             stream=None)
+    a.update(kw)
+    return L.kvattn_kv_append(a["k"], a["v"], a["sm"], a["kv"], a["nb"], a["T"], a["hkv"],
+                              a["d"], a["bs"], a["dt"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=5), K.KV_ERR_INVALID),
+    (dict(T=-1), K.KV_ERR_INVALID),
+    (dict(d=12), K.KV_ERR_INVALID),                      # 24-byte rows: not whole chunks
+    (dict(d=4, dt=K.KV_BF16), K.KV_ERR_INVALID),
+    (dict(d=8), K.KV_ERR_UNSUPPORTED),                   # 16-byte rows
+    (dict(d=320), K.KV_ERR_UNSUPPORTED),                 # 640-byte rows
+    (dict(hkv=0), K.KV_ERR_INVALID),
+    (dict(bs=32), K.KV_ERR_UNSUPPORTED),
+    (dict(nb=0), K.KV_ERR_INVALID),
+    (dict(nb=1 << 28), K.KV_ERR_INVALID),                # slots overflow int32
+    (dict(sm=0), K.KV_ERR_INVALID),
+    (dict(k=A + 4), K.KV_ERR_INVALID),                   # misaligned
+])
+def test_append_argument_checks(L, kw, code):
+    assert _append(L, **kw) == code
+    assert K.last_error().startswith("kvattn_kv_append")
+
+
+def test_append_nothing_is_ok(L):
+    assert _append(L, T=0, k=0, v=0, sm=0) == K.KV_OK
+
+
 def test_workspace_sizes():
     split = K.decode_split_tokens(4096)
     assert split % 64 == 0 and split > 0
