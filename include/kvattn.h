@@ -225,6 +225,80 @@ int kvpool_last_toggle_breakdown(const kvpool* pool, double* create_ms, double* 
 /* Decommit if needed, unmap the base handles, free the ranges. NULL is a no-op. */
 void kvpool_destroy(kvpool* pool);
 
+/* ------------------------------------------------------------------------- */
+/* Block-id pool with the elastic gate (Section 3, "Two handles, one virtual
+ * range": the top elastic block-id range is handed out only while the elastic
+ * slice is committed). Ids [0, num_base) are base blocks, ids
+ * [num_base, num_base + num_elastic) the elastic blocks at the top of every
+ * layer's range. Host memory only; not thread-safe (one scheduler drives it).
+ * Base blocks are handed out before elastic ones, lowest id first, so that as
+ * few sequences as possible hold elastic blocks when a prefill comes. */
+typedef struct kvblocks kvblocks;
+
+int kvblocks_create(int num_base_blocks, int num_elastic_blocks, kvblocks** out);
+void kvblocks_destroy(kvblocks* blocks);
+/* Admit (admit != 0) or stop handing out (admit == 0) the elastic ids. Live
+ * elastic blocks stay allocated until freed; the controller below admits and
+ * withdraws the range together with the commit and decommit. */
+int kvblocks_set_elastic(kvblocks* blocks, int admit);
+int kvblocks_is_admitted(const kvblocks* blocks);
+/* Allocate n ids into the host array ids; KV_ERR_OOM (and nothing allocated)
+ * if fewer than n admitted ids are free. */
+int kvblocks_alloc(kvblocks* blocks, int n, int32_t* ids);
+/* Free n ids; KV_ERR_INVALID (and nothing freed) if any id is not allocated
+ * or appears twice. */
+int kvblocks_free(kvblocks* blocks, int n, const int32_t* ids);
+/* Free admitted ids; ids usable now (num_gpu_blocks): num_base, plus
+ * num_elastic while admitted; allocated ids in the elastic range. */
+int kvblocks_num_free(const kvblocks* blocks);
+int kvblocks_num_admitted(const kvblocks* blocks);
+int kvblocks_live_elastic(const kvblocks* blocks);
+/* Plan a drain of the elastic range by migration: for every live elastic id
+ * (ascending) allocate a free base id; writes *n pairs from[i] -> to[i] into
+ * host arrays of room for `capacity` pairs. The caller copies each block in
+ * every layer (kvattn_copy_blocks), rewrites its block tables, and frees the
+ * `from` ids. KV_ERR_OOM (nothing allocated) if the base range has too few free
+ * ids; KV_ERR_INVALID if capacity is too small. */
+int kvblocks_plan_drain(kvblocks* blocks, int capacity, int32_t* from, int32_t* to, int* n);
+
+/* Copy whole blocks src_ids[i] -> dst_ids[i] (device int32 arrays of n) in each
+ * of num_layers layers (layers: host array of 16-B aligned device pointers, each
+ * the base of a layer of num_blocks blocks of block_bytes bytes, a multiple of
+ * 16). Pairs with an id outside [0, num_blocks), or src == dst, are skipped;
+ * destinations must be distinct and must not be sources of other pairs.
+ * Asynchronous on stream; allocates nothing. Used to drain the elastic range
+ * before a decommit (Section 3, "Controller"). */
+int kvattn_copy_blocks(void* const* layers, int num_layers, int num_blocks,
+                       size_t block_bytes, const int32_t* src_ids, const int32_t* dst_ids,
+                       int n, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* One-step-ahead toggle controller (Section 3, "Controller"). The scheduler
+ * knows its next batch before running it and calls kvctl_before_step with
+ * whether that batch contains a prefill:
+ *   - prefill next: if committed, stop admitting elastic ids and decommit
+ *     (device sync, unmap). If elastic blocks are still live it returns
+ *     KV_ERR_STATE and changes nothing: drain them (free or migrate) and call
+ *     again. Prefill runs with the reserve returned to the device.
+ *   - decode-only next: count the run of decode-only steps; after
+ *     hysteresis_steps of them, commit and admit the elastic ids. A failed
+ *     commit (KV_ERR_OOM) leaves the pool decommitted and restarts the count.
+ * *action (nullable) receives KVCTL_NONE, KVCTL_COMMIT or KVCTL_DECOMMIT and
+ * *ms (nullable) the toggle's host wall time. With pool == NULL the controller
+ * runs the same state machine without a device (the gate only). Callers that
+ * use a caching allocator should return its cached memory to the device before
+ * a step for which kvctl_would_commit() is 1 (Section 4: a recommit after a
+ * large prefill otherwise fails while the allocator holds the freed memory). */
+typedef struct kvctl kvctl;
+enum { KVCTL_NONE = 0, KVCTL_COMMIT = 1, KVCTL_DECOMMIT = 2 };
+
+int kvctl_create(kvpool* pool, kvblocks* blocks, int hysteresis_steps, kvctl** out);
+void kvctl_destroy(kvctl* ctl);
+int kvctl_before_step(kvctl* ctl, int next_has_prefill, int* action, double* ms);
+int kvctl_would_commit(const kvctl* ctl, int next_has_prefill);
+int kvctl_is_committed(const kvctl* ctl);
+int kvctl_counts(const kvctl* ctl, int* commits, int* decommits);
+
 #ifdef __cplusplus
 }
 #endif

@@ -7,4 +7,4 @@ from .paged_kv import (  # noqa: F401
     paged_decode,
     storage_to_f64,
 )
-from .append import kv_append  # noqa: F401
+from .append import copy_blocks, kv_append  # noqa: F401

@@ -56,3 +56,17 @@ def kv_append(kv_raw: np.ndarray, k_new: np.ndarray, v_new: np.ndarray,
             layer[b, 0, g, k_pos] = k_new[t, g]
             layer[b, 1, g, v_pos] = v_new[t, g]
     return out
+
+
+def copy_blocks(kv_raw: np.ndarray, src, dst, *, num_blocks: int) -> np.ndarray:
+    """Copy of the layer with block ``dst[i]`` replaced by block ``src[i]`` (as it
+    was before any copy); pairs with an id outside ``[0, num_blocks)`` or with
+    ``src == dst`` are skipped. This is how the elastic range is drained by
+    migration before a decommit (Section 3, "Controller")."""
+    out = np.array(kv_raw, copy=True)
+    before = np.asarray(kv_raw).reshape(num_blocks, -1)
+    after = out.reshape(num_blocks, -1)
+    for s, d in zip(np.asarray(src).tolist(), np.asarray(dst).tolist()):
+        if 0 <= s < num_blocks and 0 <= d < num_blocks and s != d:
+            after[d] = before[s]
+    return out

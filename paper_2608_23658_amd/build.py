@@ -21,7 +21,8 @@ LIB = os.path.join(HERE, "libkvattn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "kvpool.cpp", "decode.hip", "prefill.hip", "append.hip"]
+SOURCES = ["abi.cpp", "kvpool.cpp", "blockpool.cpp", "decode.hip", "prefill.hip", "append.hip",
+           "blocks.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           "-I", INCLUDE, "-I", CSRC]

@@ -332,3 +332,34 @@ extern "C" int kvattn_kv_append(const void* k_new, const void* v_new,
                      "kvattn_kv_append: rows must be 64 to 512 bytes in steps of 64");
   return hip_status(e, "kvattn_kv_append launch");
 }
+
+extern "C" int kvattn_copy_blocks(void* const* layers, int num_layers, int num_blocks,
+                                  size_t block_bytes, const int32_t* src_ids,
+                                  const int32_t* dst_ids, int n, void* stream) {
+  clear_error();
+  if (num_layers < 0 || n < 0 || num_blocks <= 0)
+    return set_error(KV_ERR_INVALID, "kvattn_copy_blocks: %d layers, %d pairs, %d blocks",
+                     num_layers, n, num_blocks);
+  if (block_bytes == 0 || block_bytes % 16)
+    return set_error(KV_ERR_INVALID, "kvattn_copy_blocks: block_bytes %zu not a multiple of 16",
+                     block_bytes);
+  if (n > 0x7fffffff / 2)
+    return set_error(KV_ERR_UNSUPPORTED, "kvattn_copy_blocks: too many pairs");
+  if (n == 0 || num_layers == 0) return KV_OK;
+  if (!layers || !src_ids || !dst_ids)
+    return set_error(KV_ERR_INVALID, "kvattn_copy_blocks: null pointer argument");
+  for (int l = 0; l < num_layers; ++l)
+    if (!layers[l] || !aligned16(layers[l]))
+      return set_error(KV_ERR_INVALID, "kvattn_copy_blocks: layer %d pointer null or not "
+                                       "16-byte aligned", l);
+  kvattn::CopyArgs a;
+  a.layers = layers;
+  a.num_layers = num_layers;
+  a.num_blocks = num_blocks;
+  a.n = n;
+  a.block_bytes = block_bytes;
+  a.src = src_ids;
+  a.dst = dst_ids;
+  a.stream = static_cast<hipStream_t>(stream);
+  return hip_status(kvattn::launch_copy_blocks(a), "kvattn_copy_blocks launch");
+}

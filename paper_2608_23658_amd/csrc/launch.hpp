@@ -49,6 +49,21 @@ struct AppendArgs {
   hipStream_t stream;
 };
 
+// Layer base pointers passed by value to the block-copy kernel.
+constexpr int kMaxCopyLayers = 128;
+struct CopyLayers {
+  void* p[kMaxCopyLayers];
+};
+
+struct CopyArgs {
+  void* const* layers;   // host array of num_layers device pointers
+  int num_layers, num_blocks, n;
+  size_t block_bytes;
+  const int32_t* src;
+  const int32_t* dst;
+  hipStream_t stream;
+};
+
 // Tracing hooks around each kernel launch (no-ops unless a trace is installed).
 void trace_before(hipStream_t stream, const char* kernel);
 void trace_after(hipStream_t stream);
@@ -56,6 +71,7 @@ void trace_after(hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a);
 hipError_t launch_prefill(const PrefillArgs& a);
 hipError_t launch_append(const AppendArgs& a);
+hipError_t launch_copy_blocks(const CopyArgs& a);
 
 // Query rows per prefill work tile (per query head).
 constexpr int kPrefillRows = 64;

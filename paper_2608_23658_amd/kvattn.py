@@ -13,6 +13,7 @@ import os
 import re
 from typing import Optional
 
+import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -70,6 +71,24 @@ def lib() -> ctypes.CDLL:
        ctypes.POINTER(ctypes.c_size_t))
     _c(L.kvpool_last_toggle_breakdown, i32, vp, dp, dp, dp, dp, dp)
     _c(L.kvpool_destroy, None, vp)
+    ip = ctypes.POINTER(ctypes.c_int32)
+    _c(L.kvblocks_create, i32, i32, i32, ctypes.POINTER(vp))
+    _c(L.kvblocks_destroy, None, vp)
+    _c(L.kvblocks_set_elastic, i32, vp, i32)
+    _c(L.kvblocks_is_admitted, i32, vp)
+    _c(L.kvblocks_alloc, i32, vp, i32, ip)
+    _c(L.kvblocks_free, i32, vp, i32, ip)
+    _c(L.kvblocks_num_free, i32, vp)
+    _c(L.kvblocks_num_admitted, i32, vp)
+    _c(L.kvblocks_live_elastic, i32, vp)
+    _c(L.kvblocks_plan_drain, i32, vp, i32, ip, ip, ctypes.POINTER(i32))
+    _c(L.kvattn_copy_blocks, i32, ctypes.POINTER(vp), i32, i32, sz, vp, vp, i32, vp)
+    _c(L.kvctl_create, i32, vp, vp, i32, ctypes.POINTER(vp))
+    _c(L.kvctl_destroy, None, vp)
+    _c(L.kvctl_before_step, i32, vp, i32, ctypes.POINTER(i32), dp)
+    _c(L.kvctl_would_commit, i32, vp, i32)
+    _c(L.kvctl_is_committed, i32, vp)
+    _c(L.kvctl_counts, i32, vp, ctypes.POINTER(i32), ctypes.POINTER(i32))
     _c(L.kvattn_trace_begin, i32, ctypes.POINTER(vp), i32)
     _c(L.kvattn_trace_end, i32, ctypes.POINTER(i32))
     _c(L.kvattn_trace_kernel_name, ctypes.c_char_p, i32)
@@ -322,6 +341,141 @@ class ElasticPool:
     def close(self) -> None:
         if self._h is not None and self._h.value:
             lib().kvpool_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _ids(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _iptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+class BlockPool:
+    """Block-id allocator with the elastic gate (kvblocks_* in the C ABI)."""
+
+    def __init__(self, num_base: int, num_elastic: int):
+        h = ctypes.c_void_p()
+        check(lib().kvblocks_create(int(num_base), int(num_elastic), ctypes.byref(h)))
+        self._h = h
+        self.num_base = int(num_base)
+        self.num_elastic = int(num_elastic)
+
+    def alloc(self, n: int) -> np.ndarray:
+        out = np.empty(int(n), dtype=np.int32)
+        check(lib().kvblocks_alloc(self._h, int(n), _iptr(out)))
+        return out
+
+    def free(self, ids) -> None:
+        a = _ids(ids)
+        check(lib().kvblocks_free(self._h, a.size, _iptr(a)))
+
+    def set_elastic(self, admit: bool) -> None:
+        check(lib().kvblocks_set_elastic(self._h, int(bool(admit))))
+
+    @property
+    def admitted(self) -> bool:
+        return self._int(lib().kvblocks_is_admitted(self._h)) == 1
+
+    @property
+    def num_free(self) -> int:
+        return self._int(lib().kvblocks_num_free(self._h))
+
+    @property
+    def num_admitted(self) -> int:
+        return self._int(lib().kvblocks_num_admitted(self._h))
+
+    @property
+    def live_elastic(self) -> int:
+        return self._int(lib().kvblocks_live_elastic(self._h))
+
+    def plan_drain(self):
+        """(from, to) int32 arrays: each live elastic id and the base id it moves to."""
+        cap = self.live_elastic
+        f = np.empty(max(cap, 1), dtype=np.int32)
+        t = np.empty(max(cap, 1), dtype=np.int32)
+        n = ctypes.c_int()
+        check(lib().kvblocks_plan_drain(self._h, cap, _iptr(f), _iptr(t), ctypes.byref(n)))
+        return f[:n.value].copy(), t[:n.value].copy()
+
+    @staticmethod
+    def _int(rc: int) -> int:
+        if rc < 0:
+            check(rc)
+        return rc
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            lib().kvblocks_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def copy_blocks(layers, num_blocks: int, block_bytes: int, src: torch.Tensor, dst: torch.Tensor,
+                stream=None) -> None:
+    """Copy blocks src[i] -> dst[i] (device int32) in every layer (device pointers)."""
+    _require_cuda(src, dst)
+    if src.dtype != torch.int32 or dst.dtype != torch.int32 or src.shape != dst.shape:
+        raise ValueError("src and dst must be int32 tensors of one shape")
+    ptrs = (ctypes.c_void_p * len(layers))(*[_ptr(x) for x in layers])
+    check(lib().kvattn_copy_blocks(ptrs, len(layers), int(num_blocks), int(block_bytes),
+                                   _ptr(src), _ptr(dst), int(src.numel()), _stream(stream)))
+
+
+KVCTL_NONE, KVCTL_COMMIT, KVCTL_DECOMMIT = 0, 1, 2
+
+
+class Controller:
+    """One-step-ahead commit/decommit controller (kvctl_* in the C ABI).
+
+    ``pool`` may be None: the state machine runs without a device."""
+
+    def __init__(self, pool: Optional["ElasticPool"], blocks: BlockPool, hysteresis: int):
+        h = ctypes.c_void_p()
+        check(lib().kvctl_create(pool._h if pool is not None else None, blocks._h,
+                                 int(hysteresis), ctypes.byref(h)))
+        self._h = h
+        self.pool = pool
+        self.blocks = blocks
+
+    def before_step(self, next_has_prefill: bool):
+        """Returns (action, host ms). Empties torch's cache first when the call
+        is about to commit, so memory it holds is free for the elastic handles."""
+        if self.pool is not None and lib().kvctl_would_commit(self._h, int(bool(next_has_prefill))):
+            torch.cuda.empty_cache()
+        act = ctypes.c_int()
+        ms = ctypes.c_double()
+        check(lib().kvctl_before_step(self._h, int(bool(next_has_prefill)), ctypes.byref(act),
+                                      ctypes.byref(ms)))
+        return act.value, ms.value
+
+    @property
+    def committed(self) -> bool:
+        rc = lib().kvctl_is_committed(self._h)
+        if rc < 0:
+            check(rc)
+        return rc == 1
+
+    def counts(self):
+        c, d = ctypes.c_int(), ctypes.c_int()
+        check(lib().kvctl_counts(self._h, ctypes.byref(c), ctypes.byref(d)))
+        return c.value, d.value
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            lib().kvctl_destroy(self._h)
         self._h = None
 
     def __del__(self):

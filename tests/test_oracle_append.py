@@ -114,3 +114,20 @@ def test_planted_mistakes_are_caught(mutant, monkeypatch):
         except AssertionError:
             failed += 1
     assert failed >= 1, mutant.__name__
+
+
+def test_copy_blocks_moves_whole_blocks():
+    """After copying, gathering the destination block returns the source
+    block's rows (the gather is pinned by the attention brute force), other
+    blocks are untouched, and invalid pairs are skipped."""
+    hkv, d, bs, nb = 2, 64, 16, 8
+    rng = np.random.default_rng(5)
+    layer = rng.integers(0, 1 << 16, size=nb * 2 * hkv * bs * d, dtype=np.uint16)
+    out = oracle.copy_blocks(layer, [5, 2, 9, 3], [1, 6, 0, 3], num_blocks=nb)
+    for s, t in ((5, 1), (2, 6)):
+        Ks, Vs = oracle.gather_kv(layer, "bf16", np.array([s]), bs, hkv, bs, d)
+        Kt, Vt = oracle.gather_kv(out, "bf16", np.array([t]), bs, hkv, bs, d)
+        assert np.array_equal(Ks, Kt, equal_nan=True) and np.array_equal(Vs, Vt, equal_nan=True)
+    blk = layer.reshape(nb, -1)
+    for b in (0, 2, 3, 4, 5, 7):
+        assert np.array_equal(out.reshape(nb, -1)[b], blk[b])
