@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
                     choices=["all", "decode", "prefill", "mixed", "append", "toggle", "elastic",
-                             "copy"],
+                             "necessity", "copy"],
                     help="'all' = headline decode plus the prefill, mixed-step and toggle "
                          "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
                          "scales the HBM byte counters")
@@ -291,9 +291,23 @@ def toggle_leg(K):
                                    for k in ("create_ms", "map_ms", "access_ms")},
            "decommit_breakdown_ms": {k: med([x[k] for x in bd_d])
                                      for k in ("sync_ms", "unmap_ms")}}
+    # the naive alternative: one handle for the whole reserve (allocation cost only:
+    # on ROCm such a handle cannot back the per-layer slices)
+    single = [K.ElasticPool.time_single_handle(el * ELASTIC.num_layers) for _ in range(5)]
+    res["single_handle_reserve_ms_median"] = {
+        k: med([x[k] for x in single]) for k in ("create_ms", "map_ms", "access_ms",
+                                                  "release_ms")}
     log(f"toggle: commit {res['commit_ms_median']:.2f} ms, decommit "
-        f"{res['decommit_ms_median']:.2f} ms")
+        f"{res['decommit_ms_median']:.2f} ms; one {el * ELASTIC.num_layers >> 20} MiB handle: "
+        f"{res['single_handle_reserve_ms_median']}")
     return res
+
+
+def necessity_leg():
+    from paper_2608_23658_amd import necessity
+    r = necessity.run()
+    log(f"necessity: {r}")
+    return r
 
 
 def elastic_leg(args, K, work):
@@ -485,6 +499,8 @@ def main():
                         config={"workload": "kv_append_8192x8x128_bf16"})
     if args.workload in ("all", "toggle"):
         line["elastic_toggle"] = toggle_leg(K)
+    if args.workload in ("all", "necessity"):
+        line["necessity"] = necessity_leg()
     if args.workload in ("all", "elastic"):
         line["elastic_decode"] = elastic_leg(args, K, work)
         if line["value"] is None:

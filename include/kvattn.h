@@ -225,6 +225,17 @@ int kvpool_last_toggle_breakdown(const kvpool* pool, double* create_ms, double* 
 /* Decommit if needed, unmap the base handles, free the ranges. NULL is a no-op. */
 void kvpool_destroy(kvpool* pool);
 
+/* Cost of the naive toggle (Section 3, "Toggle cost": a whole-handle commit of
+ * the entire reserve, where physical allocation dominates). On ROCm a handle
+ * maps only at offset 0, so one handle cannot back the per-layer elastic
+ * slices at all; this times what such a commit would pay for the allocation
+ * and mapping: reserve a fresh range, create one handle of `bytes` (a multiple
+ * of the granularity), map it, grant access, then unmap and release it and free
+ * the range. Host wall times in ms; any output pointer may be NULL. Returns
+ * KV_ERR_OOM if the handle cannot be created. */
+int kvpool_time_single_handle(int device, size_t bytes, double* create_ms, double* map_ms,
+                              double* access_ms, double* release_ms);
+
 /* ------------------------------------------------------------------------- */
 /* Block-id pool with the elastic gate (Section 3, "Two handles, one virtual
  * range": the top elastic block-id range is handed out only while the elastic

@@ -309,3 +309,49 @@ extern "C" void kvpool_destroy(kvpool* p) {
   if (p->committed) (void)kvpool_decommit_elastic(p, nullptr);
   free_pool(p);
 }
+
+extern "C" int kvpool_time_single_handle(int device, size_t bytes, double* create_ms,
+                                         double* map_ms, double* access_ms, double* release_ms) {
+  kvattn::clear_error();
+  size_t gran = 0;
+  int rc = kvpool_granularity(device, &gran);
+  if (rc != KV_OK) return rc;
+  if (bytes == 0 || bytes % gran)
+    return kvattn::set_error(KV_ERR_INVALID,
+                             "kvpool_time_single_handle: %zu bytes is not a multiple of %zu",
+                             bytes, gran);
+  DeviceScope scope(device);
+  if (!scope.ok) return kvattn::set_error(KV_ERR_HIP, "kvpool_time_single_handle: hipSetDevice");
+  const size_t align = gran > kHugePage ? gran : kHugePage;
+  void* va = nullptr;
+  hipError_t e = hipMemAddressReserve(&va, bytes, align, nullptr, 0);
+  if (e != hipSuccess) return hip_fail(e, "hipMemAddressReserve");
+  hipMemAllocationProp prop = device_prop(device);
+  hipMemAccessDesc acc = access_desc(device);
+  hipMemGenericAllocationHandle_t h = 0;
+  const auto t0 = clock_type::now();
+  e = hipMemCreate(&h, bytes, &prop, 0);
+  if (e != hipSuccess) {
+    (void)hipMemAddressFree(va, bytes);
+    return hip_fail(e, "hipMemCreate(single)");
+  }
+  const auto t1 = clock_type::now();
+  e = hipMemMap(va, bytes, 0, h, 0);
+  const auto t2 = clock_type::now();
+  hipError_t ea = e == hipSuccess ? hipMemSetAccess(va, bytes, &acc, 1) : e;
+  const auto t3 = clock_type::now();
+  if (e == hipSuccess) (void)hipMemUnmap(va, bytes);
+  (void)hipMemRelease(h);
+  const auto t4 = clock_type::now();
+  (void)hipMemAddressFree(va, bytes);
+  if (e != hipSuccess) return hip_fail(e, "hipMemMap(single)");
+  if (ea != hipSuccess) return hip_fail(ea, "hipMemSetAccess(single)");
+  auto ms = [](clock_type::time_point a, clock_type::time_point b) {
+    return std::chrono::duration<double, std::milli>(b - a).count();
+  };
+  if (create_ms) *create_ms = ms(t0, t1);
+  if (map_ms) *map_ms = ms(t1, t2);
+  if (access_ms) *access_ms = ms(t2, t3);
+  if (release_ms) *release_ms = ms(t3, t4);
+  return KV_OK;
+}

@@ -71,6 +71,7 @@ def lib() -> ctypes.CDLL:
        ctypes.POINTER(ctypes.c_size_t))
     _c(L.kvpool_last_toggle_breakdown, i32, vp, dp, dp, dp, dp, dp)
     _c(L.kvpool_destroy, None, vp)
+    _c(L.kvpool_time_single_handle, i32, i32, sz, dp, dp, dp, dp)
     ip = ctypes.POINTER(ctypes.c_int32)
     _c(L.kvblocks_create, i32, i32, i32, ctypes.POINTER(vp))
     _c(L.kvblocks_destroy, None, vp)
@@ -337,6 +338,13 @@ class ElasticPool:
         check(lib().kvpool_last_toggle_breakdown(self._h, *[ctypes.byref(x) for x in v]))
         return dict(zip(["create_ms", "map_ms", "access_ms", "sync_ms", "unmap_ms"],
                         [x.value for x in v]))
+
+    @staticmethod
+    def time_single_handle(nbytes: int, device: int = 0) -> dict:
+        """Create + map + access + release of one handle of nbytes (host ms)."""
+        v = [ctypes.c_double() for _ in range(4)]
+        check(lib().kvpool_time_single_handle(device, int(nbytes), *[ctypes.byref(x) for x in v]))
+        return dict(zip(["create_ms", "map_ms", "access_ms", "release_ms"], [x.value for x in v]))
 
     def close(self) -> None:
         if self._h is not None and self._h.value:
