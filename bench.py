@@ -39,8 +39,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
-                    choices=["all", "decode", "prefill", "mixed", "append", "toggle", "elastic",
-                             "necessity", "copy"],
+                    choices=["all", "decode", "prefill", "mixed", "append", "two_tensor",
+                             "toggle", "elastic", "necessity", "copy"],
                     help="'all' = headline decode plus the prefill, mixed-step and toggle "
                          "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
                          "scales the HBM byte counters")
@@ -158,6 +158,41 @@ def decode_leg(args, K, work, wl):
         "num_seqs": b.num_seqs, "sum_seq_len": int(b.seq_lens.sum()),
     }
     return res, b
+
+
+def two_tensor_leg(args, K, work, b):
+    """The decode workload with its top 15% of block ids moved into a second,
+    separately allocated tensor (the layer split the paper rejects), against
+    the one-range decode over the same bytes."""
+    q = b.q.cuda()
+    kv = b.kv_layer.cuda()
+    bt = torch.from_numpy(b.block_table).cuda()
+    sl = torch.from_numpy(b.seq_lens).cuda()
+    nb = b.num_blocks
+    nbase = int(0.85 * nb)
+    per_block = 2 * 8 * 16 * 128
+    kv_base = kv[:nbase * per_block]
+    kv_el = kv[nbase * per_block:].clone()
+    out = torch.empty_like(q)
+    ws = K.workspace(K.decode_workspace_bytes(q.shape[0], 32, 128, b.max_seq_len))
+    nbytes = work.decode_bytes(b.seq_lens, 32, 8, 128, 2)
+    res = {}
+    for name, fn in (
+            ("one_range", lambda: K.decode(q, kv, nb, bt, sl, num_kv_heads=8,
+                                           max_seq_len=b.max_seq_len, scale=b.scale, out=out,
+                                           ws=ws)),
+            ("two_tensor", lambda: K.decode_two_tensor(q, kv_base, nbase, kv_el, nb - nbase, bt,
+                                                       sl, num_kv_heads=8,
+                                                       max_seq_len=b.max_seq_len, scale=b.scale,
+                                                       out=out, ws=ws))):
+        ms, _, _ = timed(fn, args.steps, args.warmup, K, "decode_split")
+        res[name] = {"ms_per_call": ms, "gbs": nbytes / ms / 1e6}
+    res["two_tensor_slowdown"] = res["two_tensor"]["ms_per_call"] / res["one_range"]["ms_per_call"]
+    res["elastic_fraction_of_ids"] = float((b.block_table >= nbase).sum() /
+                                           (b.block_table >= 0).sum())
+    log(f"two-tensor: one range {res['one_range']['ms_per_call']:.4f} ms, two tensors "
+        f"{res['two_tensor']['ms_per_call']:.4f} ms ({res['two_tensor_slowdown']:.4f}x)")
+    return res
 
 
 def prefill_leg(args, K, work):
@@ -480,6 +515,11 @@ def main():
                           "block_size": 16, "parallelism": "none (1 GPU)"}
         line["roofline"] = dec["roofline"]
         line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms")}
+    if args.workload in ("all", "two_tensor"):
+        if dec_batch is None:
+            from workloads import config_spec, make_batch
+            dec_batch = make_batch(config_spec(2))
+        line["two_tensor_decode"] = two_tensor_leg(args, K, work, dec_batch)
     if args.workload in ("all", "prefill"):
         pre, _ = prefill_leg(args, K, work)
         line["prefill"] = pre

@@ -100,6 +100,22 @@ int kvattn_decode(const void* q, const void* kv_layer, int num_blocks,
                   int block_size, int max_blocks_per_seq, int max_seq_len, float scale,
                   kv_dtype dtype, void* workspace, size_t workspace_bytes, void* stream);
 
+/* The rejected alternative (Section 3, "The contiguity constraint": split the
+ * KV into two tensors and make the kernel read both). Same as kvattn_decode
+ * but block ids below num_base_blocks address kv_base and ids from
+ * num_base_blocks to num_base_blocks + num_elastic_blocks - 1 address
+ * kv_elastic at id - num_base_blocks; both tensors use the per-block layout
+ * above. Built for bf16 with head_dim 128 (KV_ERR_UNSUPPORTED otherwise); it
+ * exists to measure the cost of the second pointer against the one-range
+ * layer the elastic pool gives. */
+int kvattn_decode_two_tensor(const void* q, const void* kv_base, int num_base_blocks,
+                             const void* kv_elastic, int num_elastic_blocks,
+                             const int32_t* block_table, const int32_t* seq_lens, void* out,
+                             int num_seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                             int block_size, int max_blocks_per_seq, int max_seq_len,
+                             float scale, kv_dtype dtype, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* Kernel tracing. While a trace buffer is installed on the calling thread,
  * every kernel the library launches from that thread is bracketed by

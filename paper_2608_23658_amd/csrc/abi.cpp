@@ -138,6 +138,17 @@ extern "C" size_t kvattn_decode_workspace_bytes(int num_seqs, int num_q_heads, i
   return decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w) ? w.total : 0;
 }
 
+namespace {
+
+int decode_common(const char* fn, const void* q, const void* kv_layer, const void* kv2,
+                  int num_base, int num_blocks, const int32_t* block_table,
+                  const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
+                  int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
+                  int max_seq_len, float scale, kv_dtype dtype, void* workspace,
+                  size_t workspace_bytes, void* stream);
+
+}  // namespace
+
 extern "C" int kvattn_decode(const void* q, const void* kv_layer, int num_blocks,
                              const int32_t* block_table, const int32_t* seq_lens, void* out,
                              int num_seqs, int num_q_heads, int num_kv_heads, int head_dim,
@@ -145,39 +156,79 @@ extern "C" int kvattn_decode(const void* q, const void* kv_layer, int num_blocks
                              float scale, kv_dtype dtype, void* workspace,
                              size_t workspace_bytes, void* stream) {
   clear_error();
-  if (num_seqs < 0) return set_error(KV_ERR_INVALID, "kvattn_decode: num_seqs %d < 0", num_seqs);
+  return decode_common("kvattn_decode", q, kv_layer, nullptr, 0, num_blocks, block_table,
+                       seq_lens, out, num_seqs, num_q_heads, num_kv_heads, head_dim,
+                       block_size, max_blocks_per_seq, max_seq_len, scale, dtype, workspace,
+                       workspace_bytes, stream);
+}
+
+extern "C" int kvattn_decode_two_tensor(const void* q, const void* kv_base, int num_base_blocks,
+                                        const void* kv_elastic, int num_elastic_blocks,
+                                        const int32_t* block_table, const int32_t* seq_lens,
+                                        void* out, int num_seqs, int num_q_heads,
+                                        int num_kv_heads, int head_dim, int block_size,
+                                        int max_blocks_per_seq, int max_seq_len, float scale,
+                                        kv_dtype dtype, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+  clear_error();
+  if (num_base_blocks <= 0 || num_elastic_blocks <= 0 ||
+      (long long)num_base_blocks + num_elastic_blocks > 0x7fffffffLL)
+    return set_error(KV_ERR_INVALID, "kvattn_decode_two_tensor: %d base + %d elastic blocks",
+                     num_base_blocks, num_elastic_blocks);
+  if (dtype != KV_BF16 || head_dim != 128)
+    return set_error(KV_ERR_UNSUPPORTED,
+                     "kvattn_decode_two_tensor: built for bf16 with head_dim 128 only");
+  if (num_seqs > 0 && (!kv_elastic || !aligned16(kv_elastic)))
+    return set_error(KV_ERR_INVALID,
+                     "kvattn_decode_two_tensor: kv_elastic null or not 16-byte aligned");
+  return decode_common("kvattn_decode_two_tensor", q, kv_base, kv_elastic, num_base_blocks,
+                       num_base_blocks + num_elastic_blocks, block_table, seq_lens, out,
+                       num_seqs, num_q_heads, num_kv_heads, head_dim, block_size,
+                       max_blocks_per_seq, max_seq_len, scale, dtype, workspace,
+                       workspace_bytes, stream);
+}
+
+namespace {
+
+int decode_common(const char* fn, const void* q, const void* kv_layer, const void* kv2,
+                  int num_base, int num_blocks, const int32_t* block_table,
+                  const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
+                  int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
+                  int max_seq_len, float scale, kv_dtype dtype, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  if (num_seqs < 0) return set_error(KV_ERR_INVALID, "%s: num_seqs %d < 0", fn, num_seqs);
   if (dtype != KV_F32 && dtype != KV_BF16)
-    return set_error(KV_ERR_INVALID, "kvattn_decode: unknown dtype %d", (int)dtype);
+    return set_error(KV_ERR_INVALID, "%s: unknown dtype %d", fn, (int)dtype);
   if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
-    return set_error(KV_ERR_INVALID, "kvattn_decode: %d query heads over %d kv heads",
+    return set_error(KV_ERR_INVALID, "%s: %d query heads over %d kv heads", fn,
                      num_q_heads, num_kv_heads);
   if (!group_ok(num_q_heads, num_kv_heads, 8))
-    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: group size %d not built",
+    return set_error(KV_ERR_UNSUPPORTED, "%s: group size %d not built", fn,
                      num_q_heads / num_kv_heads);
   if (head_dim != 64 && !(head_dim == 128 && dtype == KV_BF16))
-    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: head_dim %d not built for %s",
+    return set_error(KV_ERR_UNSUPPORTED, "%s: head_dim %d not built for %s", fn,
                      head_dim, dtype == KV_BF16 ? "bf16" : "fp32");
   if (block_size != 16)
-    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: block_size %d not built", block_size);
+    return set_error(KV_ERR_UNSUPPORTED, "%s: block_size %d not built", fn, block_size);
   if (max_blocks_per_seq <= 0 || max_seq_len < 0 ||
       (long long)max_seq_len > (long long)max_blocks_per_seq * block_size)
     return set_error(KV_ERR_INVALID,
-                     "kvattn_decode: max_seq_len %d does not fit %d blocks of %d tokens",
+                     "%s: max_seq_len %d does not fit %d blocks of %d tokens", fn,
                      max_seq_len, max_blocks_per_seq, block_size);
-  if (num_blocks <= 0) return set_error(KV_ERR_INVALID, "kvattn_decode: num_blocks %d", num_blocks);
-  if (!std::isfinite(scale)) return set_error(KV_ERR_INVALID, "kvattn_decode: scale not finite");
+  if (num_blocks <= 0) return set_error(KV_ERR_INVALID, "%s: num_blocks %d", fn, num_blocks);
+  if (!std::isfinite(scale)) return set_error(KV_ERR_INVALID, "%s: scale not finite", fn);
   if (num_kv_heads > 65535 || num_seqs > 65535)
-    return set_error(KV_ERR_UNSUPPORTED, "kvattn_decode: grid too large");
+    return set_error(KV_ERR_UNSUPPORTED, "%s: grid too large", fn);
   if (num_seqs == 0) return KV_OK;
   if (!q || !kv_layer || !block_table || !seq_lens || !out || !workspace)
-    return set_error(KV_ERR_INVALID, "kvattn_decode: null pointer argument");
+    return set_error(KV_ERR_INVALID, "%s: null pointer argument", fn);
   if (!aligned16(q) || !aligned16(kv_layer) || !aligned16(out) || !aligned16(workspace))
-    return set_error(KV_ERR_INVALID, "kvattn_decode: q, kv_layer, out and workspace must be "
-                                     "16-byte aligned");
+    return set_error(KV_ERR_INVALID, "%s: q, kv_layer, out and workspace must be "
+                                     "16-byte aligned", fn);
   DecodeWs w;
   decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w);
   if (workspace_bytes < w.total)
-    return set_error(KV_ERR_INVALID, "kvattn_decode: workspace %zu bytes < %zu needed",
+    return set_error(KV_ERR_INVALID, "%s: workspace %zu bytes < %zu needed", fn,
                      workspace_bytes, w.total);
 
   kvattn::DecodeArgs a;
@@ -199,8 +250,14 @@ extern "C" int kvattn_decode(const void* q, const void* kv_layer, int num_blocks
   a.workspace = workspace;
   a.ws_ml_offset = w.ml_offset;
   a.stream = static_cast<hipStream_t>(stream);
-  return hip_status(kvattn::launch_decode(a), "kvattn_decode launch");
+  a.kv2 = kv2;
+  a.num_base = num_base;
+  const hipError_t e = kvattn::launch_decode(a);
+  if (e == hipErrorNotSupported) return set_error(KV_ERR_UNSUPPORTED, "%s: not built", fn);
+  return hip_status(e, fn);
 }
+
+}  // namespace
 
 extern "C" size_t kvattn_prefill_workspace_bytes(int num_seqs, int total_q_tokens,
                                                  int num_q_heads, int head_dim) {

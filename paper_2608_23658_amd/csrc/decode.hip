@@ -49,9 +49,13 @@ struct DecodeShape {
   static_assert(kVI * 1024 == kTileElems * kEsz, "V tile is kVI loads of 1 KiB");
 };
 
-template <int D, int G, bool BF16>
+// kTwo: the layer is split over two tensors (the design the paper rejects in
+// Section 3, "The contiguity constraint"): ids below num_base address kv, the
+// others kv2 at id - num_base. Otherwise kv2 and num_base are unused.
+template <int D, int G, bool BF16, bool kTwo = false>
 __global__ __launch_bounds__(64) void decode_split_kernel(
-    const uint8_t* __restrict__ q, const uint8_t* __restrict__ kv, int num_blocks,
+    const uint8_t* __restrict__ q, const uint8_t* __restrict__ kv,
+    const uint8_t* __restrict__ kv2, int num_base, int num_blocks,
     const int* __restrict__ block_table, const int* __restrict__ seq_lens,
     uint8_t* __restrict__ out, float* __restrict__ ws_o, float2* __restrict__ ws_ml,
     int num_seqs, int num_q_heads, int num_kv_heads, int max_blocks, int max_seq_len,
@@ -93,6 +97,13 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
   const size_t head_off = (size_t)g * tile_bytes;
   const size_t block_bytes = 2 * (size_t)num_kv_heads * tile_bytes;
   const size_t v_off = (size_t)num_kv_heads * tile_bytes + head_off;
+  auto block_ptr = [&](int id) -> const uint8_t* {
+    if constexpr (kTwo)
+      return id < num_base ? kv + (size_t)id * block_bytes
+                           : kv2 + (size_t)(id - num_base) * block_bytes;
+    else
+      return kv + (size_t)id * block_bytes;
+  };
 
   float m_run[G], l_run[G], acc[S::kVI][G];
 #pragma unroll
@@ -130,7 +141,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     // ---- loads: K rows (lane per token), V dim rows ----
     uint4 kreg[S::kKCh];
     if (kvalid) {
-      const uint4* kp = reinterpret_cast<const uint4*>(kv + (size_t)my_b * block_bytes + head_off) + kr;
+      const uint4* kp = reinterpret_cast<const uint4*>(block_ptr(my_b) + head_off) + kr;
 #pragma unroll
       for (int c = 0; c < S::kKCh; ++c) kreg[c] = load_nt(kp + c * S::kBS);
     } else {
@@ -141,7 +152,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
 #pragma unroll
     for (int j = 0; j < S::kTB; ++j) {
       if (bid[j] >= 0) {
-        const uint4* vp = reinterpret_cast<const uint4*>(kv + (size_t)bid[j] * block_bytes + v_off) + lane;
+        const uint4* vp = reinterpret_cast<const uint4*>(block_ptr(bid[j]) + v_off) + lane;
 #pragma unroll
         for (int i = 0; i < S::kVI; ++i) vreg[j][i] = load_nt(vp + i * kWave);
       } else {
@@ -357,7 +368,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(
   }
 }
 
-template <int D, int G, bool BF16>
+template <int D, int G, bool BF16, bool kTwo = false>
 static hipError_t launch_decode_t(const DecodeArgs& a) {
   const int max_splits = (a.max_seq_len + a.split_tokens - 1) / a.split_tokens;
   const int splits = max_splits > 0 ? max_splits : 1;
@@ -365,10 +376,11 @@ static hipError_t launch_decode_t(const DecodeArgs& a) {
   if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   float* ws_o = reinterpret_cast<float*>(a.workspace);
   float2* ws_ml = reinterpret_cast<float2*>(static_cast<uint8_t*>(a.workspace) + a.ws_ml_offset);
-  trace_before(a.stream, "decode_split");
-  hipLaunchKernelGGL((decode_split_kernel<D, G, BF16>), dim3((unsigned)blocks), dim3(64), 0,
+  trace_before(a.stream, kTwo ? "decode_split_two_tensor" : "decode_split");
+  hipLaunchKernelGGL((decode_split_kernel<D, G, BF16, kTwo>), dim3((unsigned)blocks), dim3(64), 0,
                      a.stream, static_cast<const uint8_t*>(a.q),
-                     static_cast<const uint8_t*>(a.kv), a.num_blocks, a.block_table, a.seq_lens,
+                     static_cast<const uint8_t*>(a.kv), static_cast<const uint8_t*>(a.kv2),
+                     a.num_base, a.num_blocks, a.block_table, a.seq_lens,
                      static_cast<uint8_t*>(a.out), ws_o, ws_ml, a.num_seqs, a.num_q_heads,
                      a.num_kv_heads, a.max_blocks, a.max_seq_len, a.split_tokens, splits,
                      a.scale * kLog2e);
@@ -398,6 +410,16 @@ static hipError_t dispatch_g(const DecodeArgs& a, int G) {
 
 hipError_t launch_decode(const DecodeArgs& a) {
   const int G = a.num_q_heads / a.num_kv_heads;
+  if (a.kv2) {   // two-tensor layer: built for bf16, head_dim 128
+    if (!a.bf16 || a.head_dim != 128) return hipErrorNotSupported;
+    switch (G) {
+      case 1: return launch_decode_t<128, 1, true, true>(a);
+      case 2: return launch_decode_t<128, 2, true, true>(a);
+      case 4: return launch_decode_t<128, 4, true, true>(a);
+      case 8: return launch_decode_t<128, 8, true, true>(a);
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (a.bf16) {
     if (a.head_dim == 128) return dispatch_g<128, true>(a, G);
     if (a.head_dim == 64) return dispatch_g<64, true>(a, G);

@@ -10,6 +10,8 @@ namespace kvattn {
 struct DecodeArgs {
   const void* q;
   const void* kv;
+  const void* kv2 = nullptr;   // second tensor of a two-tensor layer (ids >= num_base)
+  int num_base = 0;
   int num_blocks;
   const int32_t* block_table;
   const int32_t* seq_lens;

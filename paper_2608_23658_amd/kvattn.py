@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
     _c(L.kvattn_decode_split_tokens, i32, i32)
     _c(L.kvattn_decode, i32, vp, vp, i32, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
        i32, vp, sz, vp)
+    _c(L.kvattn_decode_two_tensor, i32, vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, i32, i32,
+       i32, i32, i32, f32, i32, vp, sz, vp)
     _c(L.kvattn_prefill_workspace_bytes, sz, i32, i32, i32, i32)
     _c(L.kvattn_prefill_chunk, i32, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
        i32, i32, i32, f32, i32, vp, sz, vp)
@@ -149,6 +151,29 @@ def decode_workspace_bytes(num_seqs: int, num_q_heads: int, head_dim: int, max_s
 
 def decode_split_tokens(max_seq_len: int) -> int:
     return int(lib().kvattn_decode_split_tokens(max_seq_len))
+
+
+def decode_two_tensor(q: torch.Tensor, kv_base, num_base: int, kv_elastic, num_elastic: int,
+                      block_table: torch.Tensor, seq_lens: torch.Tensor, *, num_kv_heads: int,
+                      max_seq_len: int, block_size: int = 16, scale: Optional[float] = None,
+                      out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Decode over a layer split into two tensors (ids >= num_base in the second)."""
+    B, Hq, d = q.shape
+    _require_cuda(q, block_table, seq_lens)
+    if out is None:
+        out = torch.empty_like(q)
+    if ws is None:
+        ws = workspace(decode_workspace_bytes(B, Hq, d, max_seq_len), q.device)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    rc = lib().kvattn_decode_two_tensor(_ptr(q), _ptr(kv_base), int(num_base), _ptr(kv_elastic),
+                                        int(num_elastic), _ptr(block_table), _ptr(seq_lens),
+                                        _ptr(out), B, Hq, int(num_kv_heads), d, int(block_size),
+                                        int(block_table.shape[1]), int(max_seq_len),
+                                        float(scale), _dtype_code(q.dtype), _ptr(ws),
+                                        ws.numel(), _stream(stream))
+    check(rc)
+    return out
 
 
 def prefill_workspace_bytes(num_seqs: int, total_q_tokens: int, num_q_heads: int,

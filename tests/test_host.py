@@ -73,6 +73,31 @@ def test_decode_argument_checks(L, kw, code):
     assert K.last_error().startswith("kvattn_decode")
 
 
+def _decode2(L, **kw):
+    a = dict(q=A, kb=A, nbase=80, ke=A, nel=20, bt=A, sl=A, out=A, B=4, hq=32, hkv=8, d=128,
+             bs=16, mb=10, msl=160, scale=0.1, dt=K.KV_BF16, ws=A, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return L.kvattn_decode_two_tensor(a["q"], a["kb"], a["nbase"], a["ke"], a["nel"], a["bt"],
+                                      a["sl"], a["out"], a["B"], a["hq"], a["hkv"], a["d"],
+                                      a["bs"], a["mb"], a["msl"], a["scale"], a["dt"], a["ws"],
+                                      a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=K.KV_F32, d=64), K.KV_ERR_UNSUPPORTED),
+    (dict(d=64), K.KV_ERR_UNSUPPORTED),
+    (dict(nel=0), K.KV_ERR_INVALID),
+    (dict(nbase=0), K.KV_ERR_INVALID),
+    (dict(ke=A + 8), K.KV_ERR_INVALID),
+    (dict(ke=0), K.KV_ERR_INVALID),
+    (dict(wsb=100), K.KV_ERR_INVALID),
+    (dict(bs=32), K.KV_ERR_UNSUPPORTED),
+])
+def test_decode_two_tensor_argument_checks(L, kw, code):
+    assert _decode2(L, **kw) == code
+    assert K.last_error().startswith("kvattn_decode_two_tensor")
+
+
 def test_decode_empty_batch_is_ok(L):
     assert _decode(L, B=0, q=0, out=0) == K.KV_OK
     assert K.last_error() == ""
