@@ -291,8 +291,10 @@ def append_leg(args, K, work):
         nbytes = work.append_bytes(T, 8, 128, 2)
         log(f"append {name}: {ms * 1e3:.1f} us/call, kernel {kern_ms * 1e3:.1f} us, "
             f"{nbytes / kern_ms / 1e6:.0f} GB/s")
+        traffic = measured_traffic({"decode_step256": "traffic_kv_append_decode256.txt",
+                                    "prefill_chunk8192": "traffic_kv_append_chunk8192.txt"}[name])
         res[name] = {"us_per_call": ms * 1e3, "kernel_us": kern_ms * 1e3,
-                     "bytes_per_call": nbytes, "roofline": roofline_hbm(nbytes, kern_ms)}
+                     "bytes_per_call": nbytes, "roofline": roofline_hbm(nbytes, kern_ms, traffic)}
     return res
 
 

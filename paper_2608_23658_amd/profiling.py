@@ -1,7 +1,9 @@
 """Turn rocprofv3 CSV output into the short text summaries kept in profiles/.
 
 ``stats``: per-kernel call count and average / total duration from a
-``--kernel-trace --stats`` run. ``traffic``: HBM bytes per launch of one
+``--kernel-trace --stats`` run; with ``--trace`` the per-dispatch trace of the
+same run is split by grid size, so that launches of one kernel on different
+workloads are averaged apart. ``traffic``: HBM bytes per launch of one
 kernel from two ``--pmc`` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
 dispatch), each scaled by what the same counter reads for a plain copy of a
 known number of bytes; the summary records a hash of the kernel's source so
@@ -75,6 +77,18 @@ def counter_per_dispatch(counter_csv: str, kernel_substr: str, counter: str,
     return list(per.values())
 
 
+def trace_by_grid(trace_csv: str) -> Dict[tuple, List[float]]:
+    """Per (kernel, grid size): the durations (ns) of its dispatches."""
+    out: Dict[tuple, List[float]] = {}
+    for r in _rows(trace_csv):
+        name = _col(r, "Kernel_Name") or ""
+        gx = int(float(_col(r, "Grid_Size_X", "Grid_Size") or 0))
+        gy = int(float(_col(r, "Grid_Size_Y") or 1))
+        dur = float(_col(r, "End_Timestamp")) - float(_col(r, "Start_Timestamp"))
+        out.setdefault((name, gx * gy), []).append(dur)
+    return out
+
+
 def cmd_stats(a) -> None:
     rows = kernel_stats(a.stats_csv)
     lines = [f"# rocprofv3 kernel stats: {a.title}", f"command = {a.command}", ""]
@@ -85,6 +99,16 @@ def cmd_stats(a) -> None:
         lines.append(f"  calls = {r['calls']}")
         lines.append(f"  average_us = {r['avg_ns'] / 1e3:.3f}")
         lines.append(f"  total_ms = {r['total_ns'] / 1e6:.3f}")
+    if a.trace:
+        lines.append("")
+        lines.append("# per grid size (threads), from the kernel trace of the same run")
+        for (name, grid), durs in sorted(trace_by_grid(a.trace).items()):
+            if a.kernel and not any(k in name for k in a.kernel):
+                continue
+            lines.append(f"kernel = {name} grid_threads = {grid}")
+            lines.append(f"  calls = {len(durs)}")
+            lines.append(f"  average_us = {statistics.fmean(durs) / 1e3:.3f}")
+            lines.append(f"  median_us = {statistics.median(durs) / 1e3:.3f}")
     _write(a.out, lines)
 
 
@@ -164,6 +188,7 @@ def main() -> None:
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
     s.add_argument("--kernel", nargs="*")
+    s.add_argument("--trace", default=None, help="the run's *_kernel_trace.csv")
     t = sub.add_parser("traffic")
     for k in ("fetch_csv", "write_csv", "copy_fetch_csv", "copy_write_csv"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
