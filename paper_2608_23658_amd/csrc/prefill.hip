@@ -380,10 +380,11 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   f32x16_t sA[2], sB[2];    // scores of even / odd steps
   bf16x8_t pA[4], pB[4];    // P of even / odd steps
 
-  // One pipeline step i: gather K of step i + 3 and V of step i + 1, then the
-  // matrix work (p.v of step i - 1, q.k of step i + 1) next to the softmax of
-  // step i. The step ends by waiting for the gathers of the earlier steps
-  // only (those of this step get the whole next step to land) and a barrier;
+  // One pipeline step i: the matrix work (p.v of step i - 1, q.k of step
+  // i + 1) next to the softmax of step i, with the gathers of K of step i + 3
+  // and V of step i + 1 in between. The step ends by waiting for the gathers
+  // of the earlier steps only (those of this step get the whole next step to
+  // land) and a barrier;
   // then O takes the rescale of step i's softmax, between the p.v of steps
   // i - 1 and i.
   //
@@ -398,9 +399,8 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
                    f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4], bf16x8_t (&p_cur)[4]) __attribute__((always_inline)) {
     constexpr bool kQK = decltype(qk_tag)::value;
     constexpr bool kPV = decltype(pv_tag)::value;
-    if (i + 3 < N) bits3 = load_half(std::false_type{}, i + 3);
-    if (i + 1 < N) load_half(std::true_type{}, i + 1);
     if (kPV && !step_clean(i - 1, bitsm1)) patch_v(i - 1, bitsm1);
+    const bool do_k = i + 3 < N, do_v = i + 1 < N;
     if (needs_mask(i, bits0)) mask_scores(i, bits0, s_cur);
 
     const int vbuf = (i + kVBufs - 1) % kVBufs;   // V of step i - 1
@@ -474,6 +474,10 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
           }
         }
       }
+      // the step's gathers, issued inside the schedule (K in slot 6, V in slot
+      // 20) so that their LDS writes do not land in one burst
+      if (k == 6 && do_k) bits3 = load_half(std::false_type{}, i + 3);
+      if (k == 20 && do_v) load_half(std::true_type{}, i + 1);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
