@@ -7,8 +7,9 @@
 // A workgroup of 8 wavefronts (two per SIMD) owns one tile: wave w serves
 // query head g * G + w % G over 32 rows. K/V steps of 64 keys (4 blocks) are
 // gathered through the block table straight into LDS (global_load_lds) once
-// per workgroup and shared by the G query heads of the group; four LDS
-// buffers let the gather run two steps ahead with one barrier per step.
+// per workgroup and shared by the G query heads of the group; three LDS
+// buffers each let K be gathered three steps and V one step ahead of their
+// use, with one barrier per step.
 //
 // Per wave and step, with v_mfma_f32_32x32x16_bf16:
 //   S^T[key][row] = K[key][:] . Q[row][:]   A = K rows read from the
@@ -169,8 +170,6 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
 
   __shared__ __attribute__((aligned(16))) uint8_t lds_k[kKBufs][kStepBlocks][kTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t lds_v[kVBufs][kStepBlocks][kTileBytes];
-  // Q^T operand of each wave: [wave][k-step][lane] 16-byte runs.
-  __shared__ __attribute__((aligned(16))) uint8_t lds_q[kWaves][8][kWave * 16];
 
   const size_t block_bytes = 2 * (size_t)num_kv_heads * kTileBytes;
   const size_t k_off = (size_t)g * kTileBytes;
@@ -187,15 +186,16 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int k_blk = ka / 2;                              // block within the key tile
   const int k_slot = 8 * kb4 + 4 * (ka % 2) + ke;        // slot within the block
 
-  // ---- Q^T operand of the wave's 32 rows, gathered into LDS ----
+  // ---- Q^T operand of the wave's 32 rows, loaded once into registers ----
   // Lane (lm, lh) of k-step ks holds dims ks * 16 + lh * 8 .. + 8 of row
   // row0 + lm; rows past the chunk read the chunk's last row (never written).
+  bf16x8_t qr[8];
   {
     const int row = min(row0 + lm, n - 1);
     const uint16_t* qrow = q + (size_t)(cu0 + row) * qstride + (size_t)h * kD + lh * 8;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      dma16(qrow + ks * 16, __builtin_amdgcn_readfirstlane(lds_addr(&lds_q[wave][ks][0])));
+      qr[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16);
   }
 
   f32x16_t oacc[4];
@@ -295,7 +295,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       for (int i = 0; i < 16; ++i) sa[kt][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
-      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(&lds_q[wave][ks][lane * 16]);
+      const bf16x8_t b = qr[ks];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const int chunk = 2 * ks + lh;
@@ -414,16 +414,11 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       return *reinterpret_cast<const bf16x8_t*>(
           &lds_k[kbuf][2 * kt + k_blk][((2 * ks + lh) * kBS + k_slot) * 16]);
     };
-    auto q_frag = [&](int ks) __attribute__((always_inline)) {
-      return *reinterpret_cast<const bf16x8_t*>(&lds_q[wave][ks][lane * 16]);
-    };
     constexpr int kAhead = 4;
     bf16x8_t fr[kAhead + 1];
-    bf16x8_t qf[3];
 #pragma unroll
     for (int k = 0; k < kAhead; ++k) {
       if (has_mfma(k)) fr[k % (kAhead + 1)] = a_frag(k);
-      if (kQK && k >= 16 && (k - 16) % 2 == 0) qf[((k - 16) / 2) % 3] = q_frag((k - 16) / 2);
     }
     float mp0 = -INFINITY, mp1 = -INFINITY, ref = 0.f, alpha = 1.f, psum = 0.f;
     bool rescale = false;
@@ -437,14 +432,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       // operand reads for slot k + kAhead
       const int kn = k + kAhead;
       if (kn < 32 && has_mfma(kn)) fr[kn % (kAhead + 1)] = a_frag(kn);
-      if (kQK && kn < 32 && kn >= 16 && (kn - 16) % 2 == 0)
-        qf[((kn - 16) / 2) % 3] = q_frag((kn - 16) / 2);
       // matrix instruction k
       if (k < 16) {
         if (kPV) oacc[k % 4] = mfma32(fr[k % (kAhead + 1)], p_prev[k / 4], oacc[k % 4]);
       } else if (kQK) {
         const int ks = (k - 16) / 2, kt = (k - 16) % 2;
-        s_nxt[kt] = mfma32(fr[k % (kAhead + 1)], qf[ks % 3], ks == 0 ? zero : s_nxt[kt]);
+        s_nxt[kt] = mfma32(fr[k % (kAhead + 1)], qr[ks], ks == 0 ? zero : s_nxt[kt]);
       }
       // softmax share of slot k
       if (k < 8) {
