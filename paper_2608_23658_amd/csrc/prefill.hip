@@ -336,45 +336,6 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   auto needs_mask = [&](int step, int bits) __attribute__((always_inline)) {
     return (step * kKeys + kKeys - 1 > wave_pos0) || !step_clean(step, bits);
   };
-  // Softmax of one step: P (bf16, 8 consecutive keys of each block), the
-  // row-sum update, and the rescale factor for O if the row's reference max
-  // moved.
-  auto sm = [&](const f32x16_t (&x)[2], bf16x8_t (&pr)[4], float& alpha, bool& rescale) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, x[kt][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float tmax = mx * scale_log2;
-    // Move the row's reference max only when its scores outgrow it by 2^8.
-    const bool grow = tmax > m_ref + kLazyRescale;
-    rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
-    const float nref = grow ? tmax : m_ref;
-    alpha = (m_ref == -INFINITY) ? 0.f : fast_exp2(m_ref - nref);
-    m_ref = nref;
-    const float ref = (nref == -INFINITY) ? 0.f : nref;
-    float psum = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      float p[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        p[i] = fast_exp2(fmaf(x[kt][i], scale_log2, -ref));
-        psum += p[i];
-      }
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const uint4 w = make_uint4(pack_bf16x2(p[8 * half + 0], p[8 * half + 1]),
-                                   pack_bf16x2(p[8 * half + 2], p[8 * half + 3]),
-                                   pack_bf16x2(p[8 * half + 4], p[8 * half + 5]),
-                                   pack_bf16x2(p[8 * half + 6], p[8 * half + 7]));
-        pr[2 * kt + half] = __builtin_bit_cast(bf16x8_t, w);
-      }
-    }
-    l_run = l_run * alpha + psum;
-  };
-
   // bitsm1, bits0 .. bits3: real-block masks of steps i - 1, i .. i + 3
   int bitsm1 = 0, bits0 = 0, bits1 = 0, bits2 = 0, bits3 = 0;
   f32x16_t sA[2], sB[2];    // scores of even / odd steps
