@@ -8,7 +8,7 @@ from tests.gpu_helpers import Dev, assert_parity, f64, oracle_decode, require_gp
 
 pytestmark = pytest.mark.gpu
 
-RAGGED = [1, 15, 16, 17, 63, 64, 65, 511, 512, 513, 1500, 2049]
+RAGGED = [1, 15, 16, 17, 63, 64, 65, 511, 512, 513, 1023, 1024, 1025, 1500, 2049, 4097]
 
 
 @pytest.fixture(scope="module", autouse=True)

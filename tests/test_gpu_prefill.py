@@ -28,6 +28,21 @@ def test_mixed_chunks_full(hq, hkv):
     assert_parity(out, oracle_prefill(b), "bf16", f"mixed {hq}/{hkv}")
 
 
+def test_sequences_without_new_rows():
+    """Sequences that add no rows in this call (n = 0, with and without cached
+    context, first, middle and last in the batch) produce nothing and leave
+    their neighbours unchanged."""
+    L = [0, 40, 300, 0, 17, 2000, 64, 500]
+    N = [0, 0, 300, 0, 17, 0, 1, 0]
+    b = make_batch_from_lens(L, N, dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=41)
+    say("prefill rowless sequences")
+    out = Dev(b).prefill()
+    torch.cuda.synchronize()
+    assert out.shape[0] == sum(N)
+    assert_parity(out, oracle_prefill(b), "bf16", "rowless sequences")
+
+
 def test_first_row_is_v0_exactly():
     b = make_batch_from_lens([70], [70], dtype="bf16", num_q_heads=32, num_kv_heads=8,
                              head_dim=128, block_size=16, seed=3, keep_contig=True)
