@@ -355,7 +355,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   // (slots 0-7: row max, slot 8: reference max and rescale factor, slots
   // 9-31: exponentials, row sum, bf16 packing). A wavefront issues in order,
   // so without this the vector work would queue behind runs of matrix
-  // instructions instead of running beside them.
+  // instructions instead of running beside them. The gathers' branches split
+  // the slots into three blocks, and the compiler moves the exponentials of
+  // slots 9-20 behind the V gather, so slots 9-20 issue their matrix
+  // instructions back to back. Holding those exponentials in their slots
+  // measured slower, and so did either strict order of the step's two halves
+  // (all matrix work first, or all softmax first).
   auto phase = [&](auto qk_tag, auto pv_tag, int i, f32x16_t (&s_cur)[2],
                    f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4], bf16x8_t (&p_cur)[4]) __attribute__((always_inline)) {
     constexpr bool kQK = decltype(qk_tag)::value;
