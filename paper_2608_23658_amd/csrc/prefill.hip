@@ -71,18 +71,21 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 
 constexpr uint32_t kBf16OnePair = 0x3f803f80u;   // (1.0, 1.0) in bf16
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes go
-// to LDS byte address lds + 16 l (lds must be wave-uniform). Issued as inline
-// assembly so that the compiler does not treat it as an LDS store that every
-// later LDS read must wait for: the callers wait for these loads themselves
-// (s_waitcnt vmcnt) before the barrier that publishes the data.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+// 16 bytes per lane from global memory straight into LDS: lane l reads
+// base + off_l and its bytes go to LDS byte address lds + 16 l (base and lds
+// must be wave-uniform). The address is given as a wave-uniform base in
+// SGPRs plus a 32-bit per-lane offset, which the memory pipeline takes in
+// fewer cycles per instruction than 64 lanes of 64-bit addresses. Issued as
+// inline assembly so that the compiler does not treat it as an LDS store
+// that every later LDS read must wait for: the callers wait for these loads
+// themselves (s_waitcnt vmcnt) before the barrier that publishes the data.
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
   asm volatile(
-      "s_mov_b32 m0, %1\n\t"
+      "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
+      "global_load_lds_dwordx4 %0, %1"
       :
-      : "v"(gptr), "s"(lds)
+      : "v"(off), "s"(base), "s"(lds)
       : "memory", "m0");
 }
 // LDS byte address of a pointer into a __shared__ array.
@@ -239,11 +242,13 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       if constexpr (kV) {
         const int vrow = pos / 2;
         const int src = vrow * 32 + (((pos % 2) ^ ((vrow >> 3) & 1)) * 16);
-        dma16(base + src, __builtin_amdgcn_readfirstlane(
-                              lds_addr(&lds_v[step % kVBufs][kb][quarter * 1024])));
+        dma16(base, (uint32_t)src,
+              __builtin_amdgcn_readfirstlane(
+                  lds_addr(&lds_v[step % kVBufs][kb][quarter * 1024])));
       } else {
-        dma16(base + pos * 16, __builtin_amdgcn_readfirstlane(
-                                   lds_addr(&lds_k[step % kKBufs][kb][quarter * 1024])));
+        dma16(base, (uint32_t)(pos * 16),
+              __builtin_amdgcn_readfirstlane(
+                  lds_addr(&lds_k[step % kKBufs][kb][quarter * 1024])));
       }
     }
     return bits;
