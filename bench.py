@@ -416,11 +416,19 @@ def elastic_leg(args, K, work):
         recommitted = per_layer_ms(bt, nb_all)
         log(f"elastic: recommitted {recommitted:.3f} ms/layer, bitwise equal {bitwise}")
         # the footprint control: the pool's layer 0 read by all 32 calls of a
-        # sweep; then the same bytes in plain torch memory
-        pool_l0 = per_layer_ms(bt, nb_all, layers=[0] * E.num_layers)
+        # sweep, and the same bytes in plain torch memory, measured in turn
+        # (pool, torch, torch, pool) so that neither gets the warmer GPU
         ctl = torch.empty(base + el, dtype=torch.uint8, device="cuda")
         ctl.copy_(pool.layer_view(0))
-        control = per_layer_ms(bt, nb_all, layers=[0] * E.num_layers, src=ctl.data_ptr())
+        l0 = [0] * E.num_layers
+        pool_runs, ctl_runs = [], []
+        for src in (None, ctl.data_ptr(), ctl.data_ptr(), None):
+            (pool_runs if src is None else ctl_runs).append(per_layer_ms(bt, nb_all, l0, src))
+        pool_l0 = statistics.median(pool_runs)
+        control = statistics.median(ctl_runs)
+        # each pool layer alone: the physical placement of a layer's pages
+        # moves its time by several percent, VMM or not
+        layer_ms = [per_layer_ms(bt, nb_all, [l] * 4) for l in range(E.num_layers)]
         ctl_equal = bool(torch.equal(outs[0].view(torch.int16), ref[0].view(torch.int16)))
         del ctl
         # toggle cycles on the full pool, no kernels in flight
@@ -441,6 +449,9 @@ def elastic_leg(args, K, work):
                           (("committed", committed), ("decommitted", decommitted),
                            ("recommitted", recommitted), ("pool_layer0_x32", pool_l0),
                            ("torch_layer0_x32", control))},
+        "layer0_x32_runs_ms": {"pool": pool_runs, "torch": ctl_runs},
+        "pool_layer_ms": {"min": min(layer_ms), "median": statistics.median(layer_ms),
+                          "max": max(layer_ms)},
         "decommitted_vs_committed_pct": 100.0 * (decommitted / committed - 1.0),
         "recommitted_bitwise_equal": bitwise, "control_bitwise_equal": ctl_equal,
         "sweep_ms_committed": committed * E.num_layers,
