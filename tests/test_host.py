@@ -203,3 +203,29 @@ def test_paper_figures_fixture():
     per_layer = fig["reserve_gib"] * 1024 / fig["num_layers"]
     assert 55 <= per_layer / fig["vmm_granularity_mib"] <= 57
     assert fig["chunk_budget_large"] // fig["chunk_budget_small"] == 4
+
+
+def test_c_client_builds_against_the_header_and_runs(tmp_path):
+    """The header is plain C99 and the library links and works from C: a small
+    client (tests/c_abi_client.c) compiled with gcc -std=c99 -pedantic -Werror
+    against include/kvattn.h and the built library makes the GPU-free calls."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    K.lib()   # the library must be built
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.dirname(K.LIB_PATH)
+    exe = str(tmp_path / "c_abi_client")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                    "-I", os.path.join(root, "include"),
+                    os.path.join(root, "tests", "c_abi_client.c"),
+                    "-L", libdir, "-l:libkvattn.so", "-Wl,-rpath," + libdir, "-o", exe],
+                   check=True, capture_output=True, text=True)
+    env = dict(os.environ)
+    env["LD_LIBRARY_PATH"] = os.pathsep.join(
+        [p for p in ("/opt/rocm/lib", env.get("LD_LIBRARY_PATH", "")) if p])
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.strip().endswith("ALL OK"), r.stdout
