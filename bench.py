@@ -258,9 +258,24 @@ def mixed_leg(args, K, work):
     flops = work.prefill_flops(b.seq_lens[:1], b.q_lens[:1], 32, 128)
     dbytes = work.decode_bytes(b.seq_lens[1:], 32, 8, 128, 2)
     log(f"mixed: {ms:.3f} ms/step, kernels {means}")
+
+    # the same step as one unified prefill call (each decode sequence a
+    # one-row chunk), as a serving engine batches it
+    cu = torch.from_numpy(b.cu_seqlens_q).cuda()
+    ou = torch.empty_like(q)
+    wsu = K.workspace(K.prefill_workspace_bytes(b.num_seqs, b.total_q_tokens, 32, 128))
+
+    def unified():
+        K.prefill_chunk(q, kv, b.num_blocks, bt, sl, cu, num_kv_heads=8,
+                        max_seq_len=b.max_seq_len, max_num_batched_tokens=8192 + 128,
+                        scale=b.scale, out=ou, ws=wsu)
+
+    ums, _, umeans = timed(unified, steps, max(1, args.warmup // 2), K, "prefill")
+    log(f"mixed, one unified call: {ums:.3f} ms/step, kernels {umeans}")
     return {"workload": spec.name, "ms_per_step": ms, "kernel_ms": means,
             "prefill_tflops": flops / (means["prefill"] * 1e-3) / 1e12,
-            "decode_gbs": dbytes / (means["decode_split"] * 1e-3) / 1e9}
+            "decode_gbs": dbytes / (means["decode_split"] * 1e-3) / 1e9,
+            "unified_call": {"ms_per_step": ums, "kernel_ms": umeans}}
 
 
 def append_leg(args, K, work):

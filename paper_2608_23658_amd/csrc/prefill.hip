@@ -170,6 +170,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int wg_rows = min(kRows, n - q0);
   const int last_pos = min(c + q0 + wg_rows - 1, L - 1);
   const int N = last_pos >= 0 ? last_pos / kKeys + 1 : 0;   // steps of the tile
+  const bool idle = row0 >= n;                  // none of the wave's 32 rows is in the chunk
 
   __shared__ __attribute__((aligned(16))) uint8_t lds_k[kKBufs][kStepBlocks][kTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t lds_v[kVBufs][kStepBlocks][kTileBytes];
@@ -193,7 +194,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   // Lane (lm, lh) of k-step ks holds dims ks * 16 + lh * 8 .. + 8 of row
   // row0 + lm; rows past the chunk read the chunk's last row (never written).
   bf16x8_t qr[8];
-  {
+  if (!idle) {
     const int row = min(row0 + lm, n - 1);
     const uint16_t* qrow = q + (size_t)(cu0 + row) * qstride + (size_t)h * kD + lh * 8;
 #pragma unroll
@@ -472,6 +473,34 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     bits1 = bits2;
     bits2 = bits3;
   };
+
+  // A wavefront none of whose rows lies in the chunk (a short chunk's last
+  // tile, a one-row decode sequence in a unified batch) still takes its share
+  // of every gather and meets every barrier, step for step like the others,
+  // but does no matrix or softmax work and writes nothing.
+  if (idle) {
+    if (N > 0) {
+      load_half(std::false_type{}, 0);
+      if (N > 1) load_half(std::false_type{}, 1);
+      if (N > 2) load_half(std::false_type{}, 2);
+      load_half(std::true_type{}, 0);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      __syncthreads();   // the others' q.k of step 0
+      for (int i = 0; i < N; ++i) {
+        if (i + 3 < N) load_half(std::false_type{}, i + 3);
+        if (i + 1 < N) load_half(std::true_type{}, i + 1);
+        if (i + 3 < N)
+          asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        else if (i + 1 < N)
+          asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+        else
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+      }
+    }
+    return;
+  }
 
   if (N > 0) {
     bits0 = load_half(std::false_type{}, 0);
