@@ -70,15 +70,25 @@ class Timer:
 
 
 def timed(fn, steps, warmup, K, kernel):
-    """Run fn warmup + steps times; returns (ms per step, mean ms of `kernel`
-    launches from per-kernel events, all per-kernel means)."""
+    """Run fn warmup + steps + steps times; returns (ms per step, mean ms of
+    `kernel` launches from per-kernel events, all per-kernel means).
+
+    The step time comes from the first `steps` runs, bracketed by
+    synchronisation, with nothing else on the stream: the library's
+    per-kernel events, recorded between its launches, leave gaps on the GPU
+    (about 15 us per decode step). The per-kernel durations come from HIP
+    events on the launch stream in a second pass of the same steps right
+    after."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    with Timer() as t:
+        for _ in range(steps):
+            fn()
     with K.KernelTrace(4 * steps) as tr:
-        with Timer() as t:
-            for _ in range(steps):
-                fn()
+        for _ in range(steps):
+            fn()
+    torch.cuda.synchronize()
     per = {}
     for name, ms in tr.durations():
         per.setdefault(name, []).append(ms)
