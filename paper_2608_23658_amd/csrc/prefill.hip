@@ -357,7 +357,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   //
   // The matrix and softmax work is laid out by hand in 32 issue slots: slot
   // k issues matrix instruction k (p.v for k < 16, q.k after), the LDS read
-  // of the operand four slots ahead, and a fixed share of the softmax
+  // of the operand five slots ahead, and a fixed share of the softmax
   // (slots 0-7: row max, slot 8: reference max and rescale factor, slots
   // 9-31: exponentials, row sum, bf16 packing). A wavefront issues in order,
   // so without this the vector work would queue behind runs of matrix
@@ -386,7 +386,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       return *reinterpret_cast<const bf16x8_t*>(
           &lds_k[kbuf][2 * kt + k_blk][((2 * ks + lh) * kBS + k_slot) * 16]);
     };
-    constexpr int kAhead = 4;
+    constexpr int kAhead = 5;
     bf16x8_t fr[kAhead + 1];
 #pragma unroll
     for (int k = 0; k < kAhead; ++k) {
