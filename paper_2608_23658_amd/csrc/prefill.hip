@@ -362,9 +362,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   // 9-31: exponentials, row sum, bf16 packing). A wavefront issues in order,
   // so without this the vector work would queue behind runs of matrix
   // instructions instead of running beside them. The gathers' branches split
-  // the slots into three blocks, and the compiler moves the exponentials of
-  // slots 9-20 behind the V gather, so slots 9-20 issue their matrix
-  // instructions back to back. Holding those exponentials in their slots
+  // the slots into three blocks, and the compiler gathers most exponentials
+  // into one run just before the V gather, so slots 10-25 issue their matrix
+  // instructions back to back. Holding the exponentials in their slots
   // measured slower, and so did either strict order of the step's two halves
   // (all matrix work first, or all softmax first).
   auto phase = [&](auto qk_tag, auto pv_tag, int i, f32x16_t (&s_cur)[2],
@@ -439,10 +439,10 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
           }
         }
       }
-      // the step's gathers, issued inside the schedule (K in slot 6, V in slot
-      // 20) so that their LDS writes do not land in one burst
-      if (k == 6 && do_k) bits3 = load_half(std::false_type{}, i + 3);
-      if (k == 20 && do_v) load_half(std::true_type{}, i + 1);
+      // the step's gathers, issued inside the schedule (K in slot 10, V in
+      // slot 26) so that their LDS writes do not land in one burst
+      if (k == 10 && do_k) bits3 = load_half(std::false_type{}, i + 3);
+      if (k == 26 && do_v) load_half(std::true_type{}, i + 1);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
