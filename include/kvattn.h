@@ -306,7 +306,11 @@ int kvattn_copy_blocks(void* const* layers, int num_layers, int num_blocks,
  *   - prefill next: if committed, stop admitting elastic ids and decommit
  *     (device sync, unmap). If elastic blocks are still live it returns
  *     KV_ERR_STATE and changes nothing: drain them (free or migrate) and call
- *     again. Prefill runs with the reserve returned to the device.
+ *     again. Prefill runs with the reserve returned to the device. If the
+ *     decommit itself fails, the error is returned and the controller takes
+ *     the pool's state: still committed after a failed device sync,
+ *     decommitted (elastic ids no longer admitted) after a failed unmap or
+ *     release.
  *   - decode-only next: count the run of decode-only steps; after
  *     hysteresis_steps of them, commit and admit the elastic ids. A failed
  *     commit (KV_ERR_OOM) leaves the pool decommitted and restarts the count.

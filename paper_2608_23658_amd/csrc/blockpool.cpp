@@ -231,7 +231,12 @@ extern "C" int kvctl_before_step(kvctl* c, int next_has_prefill, int* action, do
     if (c->pool) {
       const int rc = kvpool_decommit_elastic(c->pool, ms);
       if (rc != KV_OK) {
-        c->blocks->admitted = true;
+        // The pool's state decides: a failed device sync leaves it committed,
+        // while a failed unmap or release has already dropped the elastic
+        // handles. Elastic ids are admitted only over mapped memory.
+        c->committed = kvpool_is_committed(c->pool) == 1;
+        c->blocks->admitted = c->committed;
+        if (!c->committed) ++c->decommits;
         return rc;
       }
     }

@@ -176,12 +176,17 @@ extern "C" int kvpool_create(int device, int num_layers, size_t base_bytes_per_l
       return rc;
     }
     e = hipMemMap(p->va[l], p->base_bytes, 0, p->base_h[l], 0);
-    if (e == hipSuccess) e = hipMemSetAccess(p->va[l], p->base_bytes, &acc, 1);
     if (e != hipSuccess) {
-      rc = hip_fail(e, "hipMemMap/hipMemSetAccess(base)");
+      rc = hip_fail(e, "hipMemMap(base)");
       (void)hipMemRelease(p->base_h[l]);
       p->base_h[l] = 0;
       free_pool(p);
+      return rc;
+    }
+    e = hipMemSetAccess(p->va[l], p->base_bytes, &acc, 1);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "hipMemSetAccess(base)");
+      free_pool(p);   // layer l is mapped: free_pool unmaps and releases it
       return rc;
     }
   }
