@@ -228,7 +228,7 @@ def prefill_leg(args, K, work):
                             max_num_batched_tokens=n, scale=b.scale, out=oo, ws=ws)
 
         steps = max(3, args.steps // 5)
-        ms, kern_ms, means = timed(step, steps, max(1, args.warmup // 2), K, "prefill")
+        ms, kern_ms, means = timed(step, steps, max(5, args.warmup), K, "prefill")
         flops = work.prefill_flops([L], [n], 32, 128)
         log(f"prefill {name}: {ms:.3f} ms/call, {flops / ms / 1e9:.1f} TFLOP/s, kernels {means}")
         res[name] = {"ms_per_call": ms, "tflops": flops / (ms * 1e-3) / 1e12,
@@ -264,7 +264,7 @@ def mixed_leg(args, K, work):
                  max_seq_len=b.max_seq_len, scale=b.scale, out=od, ws=wsd)
 
     steps = max(3, args.steps // 5)
-    ms, _, means = timed(step, steps, max(1, args.warmup // 2), K, "prefill")
+    ms, _, means = timed(step, steps, max(5, args.warmup), K, "prefill")
     flops = work.prefill_flops(b.seq_lens[:1], b.q_lens[:1], 32, 128)
     dbytes = work.decode_bytes(b.seq_lens[1:], 32, 8, 128, 2)
     log(f"mixed: {ms:.3f} ms/step, kernels {means}")
@@ -280,7 +280,7 @@ def mixed_leg(args, K, work):
                         max_seq_len=b.max_seq_len, max_num_batched_tokens=8192 + 128,
                         scale=b.scale, out=ou, ws=wsu)
 
-    ums, _, umeans = timed(unified, steps, max(1, args.warmup // 2), K, "prefill")
+    ums, _, umeans = timed(unified, steps, max(5, args.warmup), K, "prefill")
     log(f"mixed, one unified call: {ums:.3f} ms/step, kernels {umeans}")
     return {"workload": spec.name, "ms_per_step": ms, "kernel_ms": means,
             "prefill_tflops": flops / (means["prefill"] * 1e-3) / 1e12,
