@@ -482,6 +482,8 @@ def elastic_leg(args, K, work):
         "layer0_x32_runs_ms": {"pool": pool_runs, "torch": ctl_runs},
         "pool_layer_ms": {"min": min(layer_ms), "median": statistics.median(layer_ms),
                           "max": max(layer_ms)},
+        "roofline_committed": roofline_hbm(
+            nbytes, committed, measured_traffic("traffic_decode_split_elastic_32l_b512.txt")),
         "decommitted_vs_committed_pct": 100.0 * (decommitted / committed - 1.0),
         "recommitted_bitwise_equal": bitwise, "control_bitwise_equal": ctl_equal,
         "sweep_ms_committed": committed * E.num_layers,
