@@ -140,9 +140,28 @@ def _stream(stream) -> int:
 
 
 def _require_cuda(*ts):
+    """Tensors reach the library as bare pointers, so they must be contiguous
+    (checked first, which also runs without a GPU) and on the GPU."""
+    for t in ts:
+        if isinstance(t, torch.Tensor) and not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
     for t in ts:
         if isinstance(t, torch.Tensor) and not t.is_cuda:
             raise ValueError("tensors must be on the GPU")
+
+
+def _require_int32(**named):
+    for name, t in named.items():
+        if t.dtype != torch.int32:
+            raise ValueError(f"{name} must be int32, not {t.dtype}")
+    bt = named.get("block_table")
+    if bt is not None and bt.dim() != 2:
+        raise ValueError("block_table must be [num_seqs, max_blocks_per_seq]")
+
+
+def _require_out(out, q):
+    if out is not None and (out.dtype != q.dtype or out.shape != q.shape):
+        raise ValueError("out must have q's shape and dtype")
 
 
 def decode_workspace_bytes(num_seqs: int, num_q_heads: int, head_dim: int, max_seq_len: int) -> int:
@@ -160,7 +179,9 @@ def decode_two_tensor(q: torch.Tensor, kv_base, num_base: int, kv_elastic, num_e
                       stream=None) -> torch.Tensor:
     """Decode over a layer split into two tensors (ids >= num_base in the second)."""
     B, Hq, d = q.shape
-    _require_cuda(q, block_table, seq_lens)
+    _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_out(out, q)
+    _require_cuda(q, kv_base, kv_elastic, block_table, seq_lens, out, ws)
     if out is None:
         out = torch.empty_like(q)
     if ws is None:
@@ -197,7 +218,9 @@ def decode(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor
     ``kv_layer`` is a tensor or a device address of the layer base.
     """
     B, Hq, d = q.shape
-    _require_cuda(q, block_table, seq_lens)
+    _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_out(out, q)
+    _require_cuda(q, kv_layer, block_table, seq_lens, out, ws)
     if out is None:
         out = torch.empty_like(q)
     if ws is None:
@@ -220,7 +243,9 @@ def prefill_chunk(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch
                   stream=None) -> torch.Tensor:
     """Chunked prefill: ``q`` [T, Hq, d] bf16, chunks given by ``cu_seqlens_q``."""
     T, Hq, d = q.shape
-    _require_cuda(q, block_table, seq_lens, cu_seqlens_q)
+    _require_int32(block_table=block_table, seq_lens=seq_lens, cu_seqlens_q=cu_seqlens_q)
+    _require_out(out, q)
+    _require_cuda(q, kv_layer, block_table, seq_lens, cu_seqlens_q, out, ws)
     B = int(seq_lens.shape[0])
     if out is None:
         out = torch.empty_like(q)
@@ -245,9 +270,7 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, slot_mapping: torch.Tens
         raise ValueError("k_new and v_new must have the same shape and dtype")
     if slot_mapping.dtype != torch.int32 or tuple(slot_mapping.shape) != (T,):
         raise ValueError("slot_mapping must be int32 [num_tokens]")
-    _require_cuda(k_new, v_new, slot_mapping)
-    if not (k_new.is_contiguous() and v_new.is_contiguous() and slot_mapping.is_contiguous()):
-        raise ValueError("k_new, v_new and slot_mapping must be contiguous")
+    _require_cuda(k_new, v_new, slot_mapping, kv_layer)
     rc = lib().kvattn_kv_append(_ptr(k_new), _ptr(v_new), _ptr(slot_mapping), _ptr(kv_layer),
                                 int(num_blocks), T, Hkv, d, int(block_size),
                                 _dtype_code(k_new.dtype), _stream(stream))
@@ -459,7 +482,7 @@ class BlockPool:
 def copy_blocks(layers, num_blocks: int, block_bytes: int, src: torch.Tensor, dst: torch.Tensor,
                 stream=None) -> None:
     """Copy blocks src[i] -> dst[i] (device int32) in every layer (device pointers)."""
-    _require_cuda(src, dst)
+    _require_cuda(src, dst, *layers)
     if src.dtype != torch.int32 or dst.dtype != torch.int32 or src.shape != dst.shape:
         raise ValueError("src and dst must be int32 tensors of one shape")
     ptrs = (ctypes.c_void_p * len(layers))(*[_ptr(x) for x in layers])

@@ -229,3 +229,25 @@ def test_c_client_builds_against_the_header_and_runs(tmp_path):
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=60)
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.strip().endswith("ALL OK"), r.stdout
+
+
+def test_binding_rejects_views_and_wide_indices_before_any_launch():
+    """Tensors reach the library as bare pointers: a strided view or an int64
+    index tensor is refused by the binding, before the library is called."""
+    import torch
+    q = torch.zeros(4, 8, 128, dtype=torch.bfloat16)
+    bt = torch.zeros(4, 3, dtype=torch.int32)
+    sl = torch.ones(4, dtype=torch.int32)
+    with pytest.raises(ValueError, match="int32"):
+        K.decode(q, 0, 10, bt.long(), sl, num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="contiguous"):
+        K.decode(q.transpose(0, 1), 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="block_table"):
+        K.decode(q, 0, 10, bt.flatten(), sl, num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="out"):
+        K.decode(q, 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48, out=q.float())
+    cu = torch.tensor([0, 1, 2, 3, 4], dtype=torch.int64)
+    with pytest.raises(ValueError, match="cu_seqlens_q"):
+        K.prefill_chunk(q, 0, 10, bt, sl, cu, num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="GPU"):
+        K.decode(q, 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48)
