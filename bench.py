@@ -139,8 +139,8 @@ def copy_leg(args):
 
 
 def decode_leg(args, K, work, wl):
-    from workloads import config_spec, make_batch
-    spec = config_spec(2)
+    from workloads import DECODE_B256, make_batch
+    spec = DECODE_B256
     log("decode: generating", spec.name)
     b = make_batch(spec)
     q = b.q.cuda()
@@ -206,8 +206,8 @@ def two_tensor_leg(args, K, work, b):
 
 
 def prefill_leg(args, K, work):
-    from workloads import config_spec, make_batch
-    spec = config_spec(4)
+    from workloads import PREFILL_L32768, make_batch
+    spec = PREFILL_L32768
     log("prefill: generating", spec.name)
     b = make_batch(spec)
     q = b.q.cuda()
@@ -241,8 +241,8 @@ def prefill_leg(args, K, work):
 def mixed_leg(args, K, work):
     """The mixed step: one prefill call (8192 new rows of a 32768-token prompt)
     and one decode call (128 sequences), back to back on one stream."""
-    from workloads import config_spec, make_batch
-    spec = config_spec(3)
+    from workloads import MIXED_STEP, make_batch
+    spec = MIXED_STEP
     log("mixed: generating", spec.name)
     b = make_batch(spec)
     q = b.q.cuda()
@@ -562,8 +562,8 @@ def main():
         line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms")}
     if args.workload in ("all", "two_tensor"):
         if dec_batch is None:
-            from workloads import config_spec, make_batch
-            dec_batch = make_batch(config_spec(2))
+            from workloads import DECODE_B256, make_batch
+            dec_batch = make_batch(DECODE_B256)
         line["two_tensor_decode"] = two_tensor_leg(args, K, work, dec_batch)
     if args.workload in ("all", "prefill"):
         pre, _ = prefill_leg(args, K, work)

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 import torch
 
-from workloads import config_spec, make_batch, make_batch_from_lens
+from workloads import DECODE_B256, TINY_DECODE_F32, make_batch, make_batch_from_lens
 from tests.gpu_helpers import Dev, assert_parity, f64, oracle_decode, require_gpu, say
 
 pytestmark = pytest.mark.gpu
@@ -16,12 +16,12 @@ def _gpu():
     require_gpu()
 
 
-def test_config1_tiny_fp32_full():
-    b = make_batch(config_spec(1))
-    say("decode config1 fp32", b.seq_lens.tolist())
+def test_tiny_decode_f32_full():
+    b = make_batch(TINY_DECODE_F32)
+    say("decode tiny fp32", b.seq_lens.tolist())
     out = Dev(b).decode()
     torch.cuda.synchronize()
-    assert_parity(out, oracle_decode(b), "f32", "config1")
+    assert_parity(out, oracle_decode(b), "f32", "tiny decode fp32")
 
 
 @pytest.mark.parametrize("hq,hkv,d,dtype", [
@@ -38,9 +38,9 @@ def test_ragged_lengths_full(hq, hkv, d, dtype):
     assert_parity(out, oracle_decode(b), dtype, f"ragged {hq}/{hkv}/{d}/{dtype}")
 
 
-def test_config2_full_size_sampled():
-    b = make_batch(config_spec(2))
-    say("decode config2 full size", b.num_seqs, int(b.seq_lens.sum()))
+def test_decode_b256_full_size_sampled():
+    b = make_batch(DECODE_B256)
+    say("decode 256 sequences, full size", b.num_seqs, int(b.seq_lens.sum()))
     out = Dev(b).decode()
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all()
@@ -48,7 +48,7 @@ def test_config2_full_size_sampled():
     seqs = sorted(set(rng.choice(b.num_seqs, 24, replace=False).tolist()
                       + [int(np.argmax(b.seq_lens)), int(np.argmin(b.seq_lens))]))
     ref = oracle_decode(b, seqs=seqs)
-    assert_parity(f64(out)[seqs], ref[seqs], "bf16", "config2 sampled")
+    assert_parity(f64(out)[seqs], ref[seqs], "bf16", "decode 256 sequences, sampled")
 
 
 def test_block_permutation_bitwise():

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 import torch
 
-from workloads import config_spec, make_batch, make_batch_from_lens
+from workloads import MIXED_STEP, PREFILL_L32768, make_batch, make_batch_from_lens
 from tests.gpu_helpers import (Dev, assert_parity, f64, oracle_decode, oracle_prefill,
                                oracle_rows, require_gpu, say)
 
@@ -77,16 +77,16 @@ def test_causality_bitwise():
     assert not torch.equal(got[p + 1:], ref[p + 1:])
 
 
-def test_config4_chunk_equivalence():
+def test_prefill_l32768_chunk_equivalence():
     """One 32768-token chunk versus four 8192-token chunks over the same cache:
     both match the oracle, and the row tiling makes them bitwise equal."""
-    b = make_batch(config_spec(4))
+    b = make_batch(PREFILL_L32768)
     d = Dev(b)
-    say("prefill config4 whole")
+    say("prefill 32768 whole")
     whole = d.prefill(max_num_batched_tokens=32768)
     parts = []
     for k in range(4):
-        say("prefill config4 chunk", k)
+        say("prefill 32768 chunk", k)
         q = d.q[8192 * k: 8192 * (k + 1)]
         sl = torch.tensor([8192 * (k + 1)], dtype=torch.int32, device="cuda")
         cu = torch.tensor([0, 8192], dtype=torch.int32, device="cuda")
@@ -100,31 +100,31 @@ def test_config4_chunk_equivalence():
     rows = sorted(set([0, 1, 63, 64, 8191, 8192, 16383, 24576, 32767]
                       + rng.choice(32768, 16, replace=False).tolist()))
     ref = oracle_rows(b, rows)
-    assert_parity(f64(whole)[rows], ref, "bf16", "config4 whole, sampled rows")
-    assert_parity(f64(chunked)[rows], ref, "bf16", "config4 4x8192, sampled rows")
+    assert_parity(f64(whole)[rows], ref, "bf16", "32768 whole, sampled rows")
+    assert_parity(f64(chunked)[rows], ref, "bf16", "32768 as 4x8192, sampled rows")
     assert torch.equal(whole.view(torch.int16), chunked.view(torch.int16))
 
 
-def test_config3_mixed_step():
+def test_mixed_step_chunk_plus_decode():
     """The last 8192-token chunk of a 32768-token prompt plus 128 decode
     sequences: as one unified call, and as a prefill call plus a decode call."""
-    b = make_batch(config_spec(3))
+    b = make_batch(MIXED_STEP)
     d = Dev(b)
-    say("prefill config3 unified")
+    say("mixed step, unified call")
     uni = d.prefill(max_num_batched_tokens=8192 + 128)
     torch.cuda.synchronize()
     rng = np.random.default_rng(2)
     rows = sorted(set([0, 1, 4095, 8191] + rng.choice(8192, 8, replace=False).tolist()
                       + (8192 + rng.choice(128, 8, replace=False)).tolist()))
     ref = oracle_rows(b, rows)
-    assert_parity(f64(uni)[rows], ref, "bf16", "config3 unified")
+    assert_parity(f64(uni)[rows], ref, "bf16", "mixed step, unified")
     # decode part alone through the decode kernel
     import paper_2608_23658_amd.kvattn as K
     qd = d.q[8192:]
-    say("decode config3 part")
+    say("mixed step, decode part")
     dec = K.decode(qd, d.kv, b.num_blocks, d.bt[1:], d.sl[1:], num_kv_heads=8,
                    max_seq_len=b.max_seq_len, scale=b.scale)
     torch.cuda.synchronize()
     drows = [r for r in rows if r >= 8192]
     assert_parity(f64(dec)[[r - 8192 for r in drows]], ref[[rows.index(r) for r in drows]],
-                  "bf16", "config3 decode part")
+                  "bf16", "mixed step, decode part")

@@ -17,7 +17,7 @@ import torch
 
 import oracle
 import oracle.paged_kv as opa
-from workloads import config_spec, make_batch, make_batch_from_lens
+from workloads import TINY_DECODE_F32, make_batch, make_batch_from_lens
 from tests.tolerance import compare
 
 
@@ -64,8 +64,8 @@ def test_bruteforce_sdpa_mixed_chunks(dtype, hq, hkv, d):
     assert np.max(np.abs(got - ref)) <= 1e-12
 
 
-def test_bruteforce_sdpa_config1_decode():
-    b = make_batch(config_spec(1), keep_contig=True)
+def test_bruteforce_sdpa_tiny_decode():
+    b = make_batch(TINY_DECODE_F32, keep_contig=True)
     got = oracle.paged_decode(b.q_raw(), b.kv_raw(), b.block_table, b.seq_lens,
                               dtype=b.dtype, num_q_heads=b.num_q_heads,
                               num_kv_heads=b.num_kv_heads, head_dim=b.head_dim,
@@ -201,7 +201,7 @@ def test_causality_future_keys_do_not_matter():
 
 
 def test_nan_poison_and_padding_never_read():
-    b = make_batch(config_spec(1))
+    b = make_batch(TINY_DECODE_F32)
     raw = b.kv_raw()
     assert np.isnan(raw).sum() > 0           # free blocks and tail slots are poisoned
     bt = b.block_table.copy()

@@ -2,7 +2,8 @@
 import numpy as np
 import torch
 
-from workloads import CONFIGS, config_spec, layout_offsets, make_batch, make_batch_from_lens
+from workloads import (DECODE_B256, MIXED_STEP, PREFILL_L32768, TINY_DECODE_F32, layout_offsets,
+                       make_batch, make_batch_from_lens)
 from workloads.configs import ELASTIC, pool_blocks_rule
 
 
@@ -40,8 +41,8 @@ def test_layout_matches_documented_offsets_f32_and_bf16():
 
 
 def test_same_seed_same_bytes_and_seed_matters():
-    a = make_batch(config_spec(1))
-    b = make_batch(config_spec(1))
+    a = make_batch(TINY_DECODE_F32)
+    b = make_batch(TINY_DECODE_F32)
     assert np.array_equal(a.kv_raw().view(np.uint32), b.kv_raw().view(np.uint32))
     assert np.array_equal(a.q_raw(), b.q_raw()) and np.array_equal(a.block_table, b.block_table)
     c = make_batch_from_lens([37, 64, 101, 130], [1] * 4, dtype="f32", num_q_heads=4,
@@ -49,8 +50,8 @@ def test_same_seed_same_bytes_and_seed_matters():
     assert not np.array_equal(a.q_raw(), c.q_raw())
 
 
-def test_config1_shapes():
-    b = make_batch(config_spec(1))
+def test_tiny_decode_shapes():
+    b = make_batch(TINY_DECODE_F32)
     assert b.seq_lens.tolist() == [37, 64, 101, 130]
     nblk = [-(-int(L) // 16) for L in b.seq_lens]
     assert sum(nblk) == 23 and b.num_blocks == 64
@@ -61,15 +62,15 @@ def test_config1_shapes():
 
 
 def test_config_length_ranges_and_pool_rule():
-    g = torch.Generator().manual_seed(CONFIGS[2].seed)
+    g = torch.Generator().manual_seed(DECODE_B256.seed)
     r = torch.randint(512, 4097, (256,), generator=g)
     assert r.min() >= 512 and r.max() <= 4096
     assert pool_blocks_rule(2048) == 2272          # 2048 * 1.1 -> 2253 -> multiple of 32
     assert pool_blocks_rule(32) == 64
-    s3 = CONFIGS[3]
+    s3 = MIXED_STEP
     assert s3.fixed_prefix == ((32768, 8192),) and s3.rand_count == 128
     assert s3.max_num_batched_tokens == 8192 + 128
-    assert CONFIGS[4].num_blocks == 2272
+    assert PREFILL_L32768.num_blocks == 2272
 
 
 def test_elastic_sizes():

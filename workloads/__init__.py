@@ -5,7 +5,9 @@ This package is shared by the CPU oracle (``oracle/``) and the HIP path
 sequence lengths, block tables, queries and keys/values from seeded
 generators and scatters the keys/values into the documented paged layout.
 """
-from .configs import CONFIGS, BatchSpec, config_spec  # noqa: F401
+from .configs import (  # noqa: F401
+    DECODE_B256, MIXED_STEP, PREFILL_L32768, TINY_DECODE_F32, WORKLOADS, BatchSpec,
+)
 from .gen import (  # noqa: F401
     PagedBatch,
     layout_offsets,

@@ -54,32 +54,28 @@ def pool_blocks_rule(total_blocks: int) -> int:
     return -(-want // 32) * 32
 
 
-CONFIGS = {
-    # Tiny paged decode in fp32: 4 sequences, GQA 2:1, head_dim 64.
-    1: BatchSpec(name="tiny_decode_f32", dtype="f32", num_q_heads=4, num_kv_heads=2,
-                 head_dim=64, block_size=16, seed=SEED_BASE + 1,
-                 fixed_seq_lens=(37, 64, 101, 130), num_blocks=64),
-    # Llama-3-8B-shaped decode layer, bf16: 256 sequences, lengths U[512, 4096].
-    2: BatchSpec(name="decode_b256_l512_4096_bf16", dtype="bf16", num_q_heads=32,
-                 num_kv_heads=8, head_dim=128, block_size=16, seed=SEED_BASE + 2,
-                 rand_count=256, rand_lo=512, rand_hi=4096),
-    # Mixed chunked-prefill step: the last 8192-token chunk of a 32768-token
-    # prompt (24576 cached tokens) plus 128 decode sequences U[1024, 8192].
-    3: BatchSpec(name="mixed_chunk8192_ctx24576_plus_decode128_bf16", dtype="bf16",
-                 num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=16,
-                 seed=SEED_BASE + 3, fixed_prefix=((32768, 8192),),
-                 rand_count=128, rand_lo=1024, rand_hi=8192,
-                 max_num_batched_tokens=8192 + 128),
-    # Chunk-size equivalence: one 32768-token prompt, prefilled whole.
-    4: BatchSpec(name="prefill_l32768_bf16", dtype="bf16", num_q_heads=32,
-                 num_kv_heads=8, head_dim=128, block_size=16, seed=SEED_BASE + 4,
-                 fixed_prefix=((32768, 32768),), num_blocks=2272,
-                 max_num_batched_tokens=32768),
-}
+# Tiny paged decode in fp32: 4 sequences, GQA 2:1, head_dim 64.
+TINY_DECODE_F32 = BatchSpec(name="tiny_decode_f32", dtype="f32", num_q_heads=4, num_kv_heads=2,
+                            head_dim=64, block_size=16, seed=SEED_BASE + 1,
+                            fixed_seq_lens=(37, 64, 101, 130), num_blocks=64)
+# Llama-3-8B-shaped decode layer, bf16: 256 sequences, lengths U[512, 4096].
+DECODE_B256 = BatchSpec(name="decode_b256_l512_4096_bf16", dtype="bf16", num_q_heads=32,
+                        num_kv_heads=8, head_dim=128, block_size=16, seed=SEED_BASE + 2,
+                        rand_count=256, rand_lo=512, rand_hi=4096)
+# Mixed chunked-prefill step: the last 8192-token chunk of a 32768-token
+# prompt (24576 cached tokens) plus 128 decode sequences U[1024, 8192].
+MIXED_STEP = BatchSpec(name="mixed_chunk8192_ctx24576_plus_decode128_bf16", dtype="bf16",
+                       num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=16,
+                       seed=SEED_BASE + 3, fixed_prefix=((32768, 8192),),
+                       rand_count=128, rand_lo=1024, rand_hi=8192,
+                       max_num_batched_tokens=8192 + 128)
+# Chunk-size equivalence: one 32768-token prompt, prefilled whole.
+PREFILL_L32768 = BatchSpec(name="prefill_l32768_bf16", dtype="bf16", num_q_heads=32,
+                           num_kv_heads=8, head_dim=128, block_size=16, seed=SEED_BASE + 4,
+                           fixed_prefix=((32768, 32768),), num_blocks=2272,
+                           max_num_batched_tokens=32768)
 
-
-def config_spec(k: int) -> BatchSpec:
-    return CONFIGS[k]
+WORKLOADS = {s.name: s for s in (TINY_DECODE_F32, DECODE_B256, MIXED_STEP, PREFILL_L32768)}
 
 
 # Elastic-pool decode workload (32 layers, base + elastic handle per layer).
