@@ -71,7 +71,8 @@ class Timer:
 
 def timed(fn, steps, warmup, K, kernel):
     """Run fn warmup + steps + steps times; returns (ms per step, mean ms of
-    `kernel` launches from per-kernel events, all per-kernel means).
+    `kernel` launches from per-kernel events, all per-kernel means, and each
+    kernel's p10 / median / p90 over its launches).
 
     The step time comes from the first `steps` runs, bracketed by
     synchronisation, with nothing else on the stream: the library's
@@ -93,7 +94,9 @@ def timed(fn, steps, warmup, K, kernel):
     for name, ms in tr.durations():
         per.setdefault(name, []).append(ms)
     means = {k: statistics.fmean(v) for k, v in per.items()}
-    return t.ms / steps, means.get(kernel), means
+    spread = {k: {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)),
+                  "p90": float(np.percentile(v, 90))} for k, v in per.items()}
+    return t.ms / steps, means.get(kernel), means, spread
 
 
 PROFILES = os.path.join(ROOT, "profiles")
@@ -154,7 +157,7 @@ def decode_leg(args, K, work, wl):
         K.decode(q, kv, b.num_blocks, bt, sl, num_kv_heads=8, max_seq_len=b.max_seq_len,
                  scale=b.scale, out=out, ws=ws)
 
-    ms, kern_ms, means = timed(step, args.steps, args.warmup, K, "decode_split")
+    ms, kern_ms, means, spread = timed(step, args.steps, args.warmup, K, "decode_split")
     nbytes = work.decode_bytes(b.seq_lens, 32, 8, 128, 2)
     kvb = work.decode_kv_bytes(b.seq_lens, 8, 128, 2)
     log(f"decode: {ms * 1e3:.1f} us/step, kernels {means}")
@@ -162,7 +165,7 @@ def decode_leg(args, K, work, wl):
         "workload": spec.name, "ms_per_step": ms,
         "gbs": nbytes / (ms * 1e-3) / 1e9,
         "kv_gbs": kvb / (ms * 1e-3) / 1e9,
-        "bytes_per_step": nbytes, "kernel_ms": means,
+        "bytes_per_step": nbytes, "kernel_ms": means, "kernel_spread_ms": spread,
         "roofline": roofline_hbm(nbytes, kern_ms,
                                  measured_traffic("traffic_decode_split_b256_l512_4096.txt")),
         "num_seqs": b.num_seqs, "sum_seq_len": int(b.seq_lens.sum()),
@@ -195,7 +198,7 @@ def two_tensor_leg(args, K, work, b):
                                                        sl, num_kv_heads=8,
                                                        max_seq_len=b.max_seq_len, scale=b.scale,
                                                        out=out, ws=ws))):
-        ms, _, _ = timed(fn, args.steps, args.warmup, K, "decode_split")
+        ms, _, _, _ = timed(fn, args.steps, args.warmup, K, "decode_split")
         res[name] = {"ms_per_call": ms, "gbs": nbytes / ms / 1e6}
     res["two_tensor_slowdown"] = res["two_tensor"]["ms_per_call"] / res["one_range"]["ms_per_call"]
     res["elastic_fraction_of_ids"] = float((b.block_table >= nbase).sum() /
@@ -228,11 +231,12 @@ def prefill_leg(args, K, work):
                             max_num_batched_tokens=n, scale=b.scale, out=oo, ws=ws)
 
         steps = max(3, args.steps // 5)
-        ms, kern_ms, means = timed(step, steps, max(5, args.warmup), K, "prefill")
+        ms, kern_ms, means, spread = timed(step, steps, max(5, args.warmup), K, "prefill")
         flops = work.prefill_flops([L], [n], 32, 128)
         log(f"prefill {name}: {ms:.3f} ms/call, {flops / ms / 1e9:.1f} TFLOP/s, kernels {means}")
         res[name] = {"ms_per_call": ms, "tflops": flops / (ms * 1e-3) / 1e12,
                      "flops_per_call": flops, "kernel_ms": means,
+                     "kernel_spread_ms": spread,
                      "roofline": roofline_mfma(flops, kern_ms, measured_traffic(
                          f"traffic_prefill_{name}.txt"))}
     return res, b
@@ -264,7 +268,7 @@ def mixed_leg(args, K, work):
                  max_seq_len=b.max_seq_len, scale=b.scale, out=od, ws=wsd)
 
     steps = max(3, args.steps // 5)
-    ms, _, means = timed(step, steps, max(5, args.warmup), K, "prefill")
+    ms, _, means, _ = timed(step, steps, max(5, args.warmup), K, "prefill")
     flops = work.prefill_flops(b.seq_lens[:1], b.q_lens[:1], 32, 128)
     dbytes = work.decode_bytes(b.seq_lens[1:], 32, 8, 128, 2)
     log(f"mixed: {ms:.3f} ms/step, kernels {means}")
@@ -280,7 +284,7 @@ def mixed_leg(args, K, work):
                         max_seq_len=b.max_seq_len, max_num_batched_tokens=8192 + 128,
                         scale=b.scale, out=ou, ws=wsu)
 
-    ums, _, umeans = timed(unified, steps, max(5, args.warmup), K, "prefill")
+    ums, _, umeans, _ = timed(unified, steps, max(5, args.warmup), K, "prefill")
     log(f"mixed, one unified call: {ums:.3f} ms/step, kernels {umeans}")
     return {"workload": spec.name, "ms_per_step": ms, "kernel_ms": means,
             "prefill_tflops": flops / (means["prefill"] * 1e-3) / 1e12,
@@ -312,7 +316,7 @@ def append_leg(args, K, work):
         def step():
             K.kv_append(k, v, sm, layer, nb)
 
-        ms, kern_ms, _ = timed(step, args.steps, args.warmup, K, "kv_append")
+        ms, kern_ms, _, spread = timed(step, args.steps, args.warmup, K, "kv_append")
         # A call is this one launch. For a kernel of ~10 us the events around
         # each launch add about 2 us, more than the back-to-back launches
         # leave between them, so the per-call time of the timed loop (launch
@@ -324,6 +328,7 @@ def append_leg(args, K, work):
         traffic = measured_traffic({"decode_step256": "traffic_kv_append_decode256.txt",
                                     "prefill_chunk8192": "traffic_kv_append_chunk8192.txt"}[name])
         res[name] = {"us_per_call": ms * 1e3, "kernel_us": kern_ms * 1e3,
+                     "kernel_spread_ms": spread,
                      "bytes_per_call": nbytes, "roofline": roofline_hbm(nbytes, dur_ms, traffic)}
     return res
 
@@ -559,7 +564,8 @@ def main():
                           "num_q_heads": 32, "num_kv_heads": 8, "head_dim": 128,
                           "block_size": 16, "parallelism": "none (1 GPU)"}
         line["roofline"] = dec["roofline"]
-        line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms")}
+        line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms",
+                                              "kernel_spread_ms")}
     if args.workload in ("all", "two_tensor"):
         if dec_batch is None:
             from workloads import DECODE_B256, make_batch
