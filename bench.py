@@ -94,8 +94,9 @@ def timed(fn, steps, warmup, K, kernel):
     for name, ms in tr.durations():
         per.setdefault(name, []).append(ms)
     means = {k: statistics.fmean(v) for k, v in per.items()}
-    spread = {k: {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)),
-                  "p90": float(np.percentile(v, 90))} for k, v in per.items()}
+    spread = {k: {"p10": round(float(np.percentile(v, 10)), 6),
+                  "median": round(float(np.median(v)), 6),
+                  "p90": round(float(np.percentile(v, 90)), 6)} for k, v in per.items()}
     return t.ms / steps, means.get(kernel), means, spread
 
 
