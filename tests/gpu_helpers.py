@@ -71,8 +71,28 @@ def f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().double().numpy()
 
 
-def assert_parity(got, ref, dtype, what=""):
-    r = compare(f64(got) if isinstance(got, torch.Tensor) else got, ref, dtype)
+def assert_parity(got, ref, dtype, what="", bounds=None):
+    """The tolerance gate over the whole output; with ``bounds`` (row offsets
+    of the sequences: ``cu_seqlens_q`` for prefill, ``0..B`` for decode) also
+    over each sequence's rows on their own, so that the large outputs of short
+    sequences cannot hide an error in the small outputs of long ones."""
+    got = f64(got) if isinstance(got, torch.Tensor) else got
+    r = compare(got, ref, dtype)
     say(what, f"max_abs={r['max_abs']:.3e} rel_l2={r['rel_l2']:.3e}")
     assert r["pass"], (what, r)
+    if bounds is not None:
+        worst = 0.0
+        for s in range(len(bounds) - 1):
+            lo, hi = int(bounds[s]), int(bounds[s + 1])
+            if hi == lo:
+                continue
+            rs = compare(got[lo:hi], ref[lo:hi], dtype)
+            assert rs["pass"], (what, "sequence", s, rs)
+            worst = max(worst, rs["rel_l2"])
+        say(what, f"worst sequence rel_l2={worst:.3e}")
     return r
+
+
+def seq_bounds(b, decode=False):
+    """Row offsets of each sequence's outputs in a batch's result."""
+    return np.arange(len(b.seq_lens) + 1) if decode else b.cu_seqlens_q

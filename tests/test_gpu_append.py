@@ -10,7 +10,7 @@ import oracle
 import paper_2608_23658_amd.kvattn as K
 from workloads import make_batch_from_lens
 from workloads.append import make_append, next_slots
-from tests.gpu_helpers import Dev, assert_parity, oracle_decode, oracle_prefill, require_gpu, say
+from tests.gpu_helpers import seq_bounds, Dev, assert_parity, oracle_decode, oracle_prefill, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -83,7 +83,8 @@ def test_decode_step_writes_its_token_then_attends():
         oracle.kv_append(b.kv_raw(), a.k_raw(), a.v_raw(), slots, dtype="bf16",
                          num_kv_heads=8, head_dim=128, block_size=16).view(np.int16)
     ).view(torch.bfloat16)
-    assert_parity(out, oracle_decode(b), "bf16", "decode after append")
+    assert_parity(out, oracle_decode(b), "bf16", "decode after append",
+                  seq_bounds(b, decode=True))
 
 
 def test_prompt_prefilled_chunk_by_chunk_with_append():

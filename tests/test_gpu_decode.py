@@ -4,7 +4,7 @@ import pytest
 import torch
 
 from workloads import DECODE_B256, TINY_DECODE_F32, make_batch, make_batch_from_lens
-from tests.gpu_helpers import Dev, assert_parity, f64, oracle_decode, require_gpu, say
+from tests.gpu_helpers import seq_bounds, Dev, assert_parity, f64, oracle_decode, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -21,7 +21,7 @@ def test_tiny_decode_f32_full():
     say("decode tiny fp32", b.seq_lens.tolist())
     out = Dev(b).decode()
     torch.cuda.synchronize()
-    assert_parity(out, oracle_decode(b), "f32", "tiny decode fp32")
+    assert_parity(out, oracle_decode(b), "f32", "tiny decode fp32", seq_bounds(b, decode=True))
 
 
 @pytest.mark.parametrize("hq,hkv,d,dtype", [
@@ -35,7 +35,8 @@ def test_ragged_lengths_full(hq, hkv, d, dtype):
     say("decode ragged", hq, hkv, d, dtype)
     out = Dev(b).decode()
     torch.cuda.synchronize()
-    assert_parity(out, oracle_decode(b), dtype, f"ragged {hq}/{hkv}/{d}/{dtype}")
+    assert_parity(out, oracle_decode(b), dtype, f"ragged {hq}/{hkv}/{d}/{dtype}",
+                  seq_bounds(b, decode=True))
 
 
 def test_decode_b256_full_size_sampled():

@@ -7,7 +7,7 @@ import torch
 
 import paper_2608_23658_amd.kvattn as K
 from workloads import make_batch_from_lens
-from tests.gpu_helpers import Dev, assert_parity, oracle_decode, require_gpu, say
+from tests.gpu_helpers import seq_bounds, Dev, assert_parity, oracle_decode, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -83,7 +83,8 @@ def test_decode_over_base_and_elastic_ids_and_bit_identical_toggle():
         say("pool decode committed")
         out1 = d.decode().clone()
         torch.cuda.synchronize()
-        assert_parity(out1, oracle_decode(b), "bf16", "pool decode, base + elastic ids")
+        assert_parity(out1, oracle_decode(b), "bf16", "pool decode, base + elastic ids",
+                      seq_bounds(b, decode=True))
         say("pool decommit / recommit")
         pool.decommit()
         pool.commit()

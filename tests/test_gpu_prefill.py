@@ -4,7 +4,7 @@ import pytest
 import torch
 
 from workloads import MIXED_STEP, PREFILL_L32768, make_batch, make_batch_from_lens
-from tests.gpu_helpers import (Dev, assert_parity, f64, oracle_decode, oracle_prefill,
+from tests.gpu_helpers import (seq_bounds, Dev, assert_parity, f64, oracle_decode, oracle_prefill,
                                oracle_rows, require_gpu, say)
 
 pytestmark = pytest.mark.gpu
@@ -25,7 +25,7 @@ def test_mixed_chunks_full(hq, hkv):
     say("prefill mixed", hq, hkv)
     out = Dev(b).prefill()
     torch.cuda.synchronize()
-    assert_parity(out, oracle_prefill(b), "bf16", f"mixed {hq}/{hkv}")
+    assert_parity(out, oracle_prefill(b), "bf16", f"mixed {hq}/{hkv}", seq_bounds(b))
 
 
 def test_sequences_without_new_rows():
@@ -40,7 +40,7 @@ def test_sequences_without_new_rows():
     out = Dev(b).prefill()
     torch.cuda.synchronize()
     assert out.shape[0] == sum(N)
-    assert_parity(out, oracle_prefill(b), "bf16", "rowless sequences")
+    assert_parity(out, oracle_prefill(b), "bf16", "rowless sequences", seq_bounds(b))
 
 
 def test_first_row_is_v0_exactly():

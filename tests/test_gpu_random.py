@@ -6,7 +6,7 @@ import pytest
 import torch
 
 from workloads import make_batch_from_lens
-from tests.gpu_helpers import Dev, assert_parity, oracle_decode, oracle_prefill, require_gpu, say
+from tests.gpu_helpers import seq_bounds, Dev, assert_parity, oracle_decode, oracle_prefill, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -35,7 +35,8 @@ def test_decode_random(seed):
                              head_dim=d, block_size=16, seed=2000 + seed)
     out = Dev(b).decode()
     torch.cuda.synchronize()
-    assert_parity(out, oracle_decode(b), dtype, f"decode random {seed}")
+    assert_parity(out, oracle_decode(b), dtype, f"decode random {seed}",
+                  seq_bounds(b, decode=True))
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -54,4 +55,4 @@ def test_prefill_random(seed):
     out = Dev(b).prefill()
     torch.cuda.synchronize()
     assert out.shape[0] == sum(n)
-    assert_parity(out, oracle_prefill(b), "bf16", f"prefill random {seed}")
+    assert_parity(out, oracle_prefill(b), "bf16", f"prefill random {seed}", seq_bounds(b))

@@ -7,7 +7,7 @@ import torch
 
 import paper_2608_23658_amd.kvattn as K
 from workloads import make_batch_from_lens
-from tests.gpu_helpers import Dev, assert_parity, oracle_decode, require_gpu, say
+from tests.gpu_helpers import seq_bounds, Dev, assert_parity, oracle_decode, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -36,4 +36,4 @@ def test_two_tensor_equals_one_range_bitwise(hq, split):
                               num_kv_heads=8, max_seq_len=b.max_seq_len, scale=b.scale)
     torch.cuda.synchronize()
     assert torch.equal(one.view(torch.int16), two.view(torch.int16))
-    assert_parity(two, oracle_decode(b), "bf16", "two-tensor decode")
+    assert_parity(two, oracle_decode(b), "bf16", "two-tensor decode", seq_bounds(b, decode=True))

@@ -322,3 +322,25 @@ def test_tolerance_negative_controls():
                                        num_kv_heads=2, head_dim=128, block_size=16,
                                        scale=b.scale)
         assert not compare(wrong, ref, "bf16")["pass"], variant
+
+
+def test_per_sequence_gate_catches_what_the_whole_output_hides():
+    """A 1-token sequence (output exactly v0, of unit size) next to a long one
+    (output of size about 1/sqrt(L)): a 5% error in the long sequence's output,
+    as a wrong normalisation would give, passes the gate over the whole output
+    and fails it per sequence."""
+    from tests.gpu_helpers import assert_parity
+    lens = [1, 2000]
+    b = make_batch_from_lens(lens, [1] * len(lens), dtype="bf16", num_q_heads=8,
+                             num_kv_heads=2, head_dim=128, block_size=16, seed=81)
+    ref = oracle.paged_decode(b.q_raw(), b.kv_raw(), b.block_table, b.seq_lens, dtype="bf16",
+                              num_q_heads=8, num_kv_heads=2, head_dim=128, block_size=16,
+                              scale=b.scale)
+    wrong = ref.copy()
+    wrong[1] *= 1.05
+    assert compare(wrong, ref, "bf16")["pass"]            # hidden by the short row
+    assert not compare(wrong[1:], ref[1:], "bf16")["pass"]
+    bounds = np.arange(len(lens) + 1)
+    with pytest.raises(AssertionError):
+        assert_parity(wrong, ref, "bf16", "negative control", bounds)
+    assert_parity(ref, ref, "bf16", "positive control", bounds)
