@@ -17,11 +17,16 @@
 //       The A rows of a 32-key tile are loaded in a permuted key order so
 //       that the accumulator of each lane ends up holding 8 consecutive keys
 //       of each of the two blocks for one query row;
-//   softmax over keys in the log2 domain: a row's 64 scores live in two
-//       lanes (l and l + 32), so the row max needs one exchange; the row
-//       state is lane-local. The running max is only moved, and O^T and the
-//       row sum rescaled, when a row's max grows by more than 2^8: the
-//       exponentials stay below 256, which bf16 P and fp32 accumulation hold;
+//   softmax over keys in the log2 domain against a per-row reference (a
+//       past row max): a row's 64 scores live in two lanes (l and l + 32)
+//       and the row state is lane-local. The reference is only moved, and
+//       O^T and the row sum rescaled, when the row's max grows past it by
+//       more than 2^8, so every exponential stays below 256, which bf16 P
+//       and fp32 accumulation hold. A lane's exponentials are at most its
+//       partial row sum, so a step whose partial sums all stay within 2^8
+//       (nearly every step after the first) needs no row max at all; the
+//       others take the exact max (one exchange between the row's two
+//       lanes) and recompute the step's exponentials;
 //   O^T[d][row] += V^T[d][key] P^T[key][row]   A = 16-byte runs of the
 //       dim-major V tile, B = the bf16 P values of 8 consecutive keys of one
 //       block, already in the lane that produced them.
@@ -49,6 +54,7 @@ constexpr int kKeys = 64;                  // keys per step
 constexpr int kStepBlocks = 4;             // blocks per step
 constexpr int kTileBytes = kBS * kD * 2;   // one (block, K/V, head) tile: 4 KiB
 constexpr float kLazyRescale = 8.f;        // log2 headroom before the max moves
+constexpr float kPsumBound = 256.f;         // 2^kLazyRescale
 constexpr int kKBufs = 3;                  // LDS K steps (gathered three steps ahead)
 constexpr int kVBufs = 3;                  // LDS V steps (gathered one step ahead)
 constexpr int kWaves = 8;                  // wavefronts per workgroup
@@ -140,7 +146,7 @@ __global__ __launch_bounds__(256) void prefill_tile_map_kernel(const int* __rest
   if (tid == 255) *count = min(scan[255], max_tiles);
 }
 
-template <int G>
+template <int G, bool kPow2Blocks>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2)))
 void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ kv,
@@ -176,6 +182,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   __shared__ __attribute__((aligned(16))) uint8_t lds_v[kVBufs][kStepBlocks][kTileBytes];
 
   const size_t block_bytes = 2 * (size_t)num_kv_heads * kTileBytes;
+  // log2 of the block size when it is a power of two (a shift replaces the
+  // 64-bit multiply in every gather's address)
+  const int block_shift = kPow2Blocks ? __builtin_ctzll(block_bytes) : 0;
   const size_t k_off = (size_t)g * kTileBytes;
   const size_t v_off = (size_t)(num_kv_heads + g) * kTileBytes;
   const int* bt = block_table + (size_t)s * max_blocks;
@@ -238,7 +247,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       const int kb = (wave + kWaves * j) / 4;     // wave-uniform
       const int quarter = (wave + kWaves * j) % 4;
       const int id = block_id(kb);
-      const uint8_t* base = kv + (size_t)(id >= 0 ? id : 0) * block_bytes + (kV ? v_off : k_off);
+      const size_t id0 = (size_t)(id >= 0 ? id : 0);
+      const uint8_t* base =
+          kv + (kPow2Blocks ? id0 << block_shift : id0 * block_bytes) + (kV ? v_off : k_off);
       const int pos = quarter * kWave + ln;       // 16-byte position in the tile
       if constexpr (kV) {
         const int vrow = pos / 2;
@@ -357,16 +368,15 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   //
   // The matrix and softmax work is laid out by hand in 32 issue slots: slot
   // k issues matrix instruction k (p.v for k < 16, q.k after), the LDS read
-  // of the operand five slots ahead, and a fixed share of the softmax
-  // (slots 0-7: row max, slot 8: reference max and rescale factor, slots
-  // 9-31: exponentials, row sum, bf16 packing). A wavefront issues in order,
-  // so without this the vector work would queue behind runs of matrix
-  // instructions instead of running beside them. The gathers' branches split
-  // the slots into three blocks, and the compiler gathers most exponentials
-  // into one run just before the V gather, so slots 10-25 issue their matrix
-  // instructions back to back. Holding the exponentials in their slots
-  // measured slower, and so did either strict order of the step's two halves
-  // (all matrix work first, or all softmax first).
+  // of the operand five slots ahead, and one exponential with its share of
+  // the row sum and bf16 packing. A wavefront issues in order, so without
+  // this the vector work would queue behind runs of matrix instructions
+  // instead of running beside them. The gathers' branches split the slots
+  // into three blocks, and the compiler gathers most exponentials of a block
+  // into one run, so some slots issue their matrix instructions back to back.
+  // Holding the exponentials in their slots measured slower, and so did
+  // either strict order of the step's two halves (all matrix work first, or
+  // all softmax first). The row max, when a step needs it, follows the slots.
   auto phase = [&](auto qk_tag, auto pv_tag, int i, f32x16_t (&s_cur)[2],
                    f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4], bf16x8_t (&p_cur)[4]) __attribute__((always_inline)) {
     constexpr bool kQK = decltype(qk_tag)::value;
@@ -392,7 +402,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     for (int k = 0; k < kAhead; ++k) {
       if (has_mfma(k)) fr[k % (kAhead + 1)] = a_frag(k);
     }
-    float mp0 = -INFINITY, mp1 = -INFINITY, ref = 0.f, alpha = 1.f, psum = 0.f;
+    float ref = (m_ref == -INFINITY) ? 0.f : m_ref, alpha = 1.f, psum = 0.f;
     bool rescale = false;
     float pe[32];
     uint32_t pw[16];
@@ -411,32 +421,15 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
         const int ks = (k - 16) / 2, kt = (k - 16) % 2;
         s_nxt[kt] = mfma32(fr[k % (kAhead + 1)], qr[ks], ks == 0 ? zero : s_nxt[kt]);
       }
-      // softmax share of slot k
-      if (k < 8) {
-        const int e = 4 * k;
-        mp0 = max3f(mp0, s_cur[e / 16][e % 16], s_cur[e / 16][e % 16 + 1]);
-        mp1 = max3f(mp1, s_cur[e / 16][e % 16 + 2], s_cur[e / 16][e % 16 + 3]);
-      } else if (k == 8) {
-        float mx = max3f(mp0, mp1, mp1);
-        mx = max3f(mx, __shfl_xor(mx, 32, kWave), mx);
-        const float tmax = mx * scale_log2;
-        // Move the row's reference max only when its scores outgrow it by 2^8.
-        const bool grow = tmax > m_ref + kLazyRescale;
-        rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
-        const float nref = grow ? tmax : m_ref;
-        alpha = (m_ref == -INFINITY) ? 0.f : fast_exp2(m_ref - nref);
-        m_ref = nref;
-        ref = (nref == -INFINITY) ? 0.f : nref;
-      } else {
-        const int e0 = ((k - 9) * 32) / 23, e1 = ((k - 8) * 32) / 23;
-#pragma unroll
-        for (int e = e0; e < e1; ++e) {
-          pe[e] = fast_exp2(fmaf(s_cur[e / 16][e % 16], scale_log2, -ref));
-          if (e % 2 == 1) {
-            // the row sum adds the bf16 values that p.v multiplies
-            pw[e / 2] = pack_bf16x2(pe[e - 1], pe[e]);
-            psum = dot2_bf16(pw[e / 2], kBf16OnePair, psum);
-          }
+      // softmax share of slot k: the exponential of score k against the
+      // current reference
+      {
+        const int e = k;
+        pe[e] = fast_exp2(fmaf(s_cur[e / 16][e % 16], scale_log2, -ref));
+        if (e % 2 == 1) {
+          // the row sum adds the bf16 values that p.v multiplies
+          pw[e / 2] = pack_bf16x2(pe[e - 1], pe[e]);
+          psum = dot2_bf16(pw[e / 2], kBf16OnePair, psum);
         }
       }
       // the step's gathers, issued inside the schedule (K in slot 10, V in
@@ -444,6 +437,35 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       if (k == 10 && do_k) bits3 = load_half(std::false_type{}, i + 3);
       if (k == 26 && do_v) load_half(std::true_type{}, i + 1);
       __builtin_amdgcn_sched_barrier(0);
+    }
+    // A row without a reference yet, or a lane whose partial row sum (which
+    // bounds each of its exponentials) left 2^8: take the exact row max, move
+    // the reference of the rows that outgrew theirs by more than 2^8, and
+    // redo the step's exponentials against it. Rows that did not outgrow
+    // theirs get the same values again.
+    if (__builtin_amdgcn_ballot_w64(m_ref == -INFINITY || !(psum <= kPsumBound)) != 0) {
+      float mp0 = -INFINITY, mp1 = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 32; e += 4) {
+        mp0 = max3f(mp0, s_cur[e / 16][e % 16], s_cur[e / 16][e % 16 + 1]);
+        mp1 = max3f(mp1, s_cur[e / 16][e % 16 + 2], s_cur[e / 16][e % 16 + 3]);
+      }
+      float mx = max3f(mp0, mp1, mp1);
+      mx = max3f(mx, __shfl_xor(mx, 32, kWave), mx);
+      const float tmax = mx * scale_log2;
+      const bool grow = tmax > m_ref + kLazyRescale;
+      rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+      const float nref = grow ? tmax : m_ref;
+      alpha = (m_ref == -INFINITY) ? 0.f : fast_exp2(m_ref - nref);
+      m_ref = nref;
+      ref = (nref == -INFINITY) ? 0.f : nref;
+      psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 32; e += 2) {
+        pw[e / 2] = pack_bf16x2(fast_exp2(fmaf(s_cur[e / 16][e % 16], scale_log2, -ref)),
+                                fast_exp2(fmaf(s_cur[e / 16][e % 16 + 1], scale_log2, -ref)));
+        psum = dot2_bf16(pw[e / 2], kBf16OnePair, psum);
+      }
     }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
@@ -577,7 +599,9 @@ static hipError_t launch_prefill_t(const PrefillArgs& a) {
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   trace_before(a.stream, "prefill");
-  hipLaunchKernelGGL((prefill_kernel<G>), dim3((unsigned)blocks), dim3(kThreads), 0, a.stream,
+  const unsigned kvh = (unsigned)a.num_kv_heads;
+  auto kernel = (kvh & (kvh - 1)) == 0 ? prefill_kernel<G, true> : prefill_kernel<G, false>;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), 0, a.stream,
                      static_cast<const uint16_t*>(a.q), static_cast<const uint8_t*>(a.kv),
                      a.num_blocks, a.block_table, a.seq_lens, a.cu_seqlens_q,
                      static_cast<uint16_t*>(a.out), tiles, count, a.num_q_heads,

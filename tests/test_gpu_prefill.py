@@ -18,7 +18,9 @@ def _gpu():
     require_gpu()
 
 
-@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (4, 1)])
+# (24, 6) and (6, 3): kv head counts that are not powers of two, so the block
+# size is not either and block offsets take the multiply path
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (4, 1), (24, 6), (6, 3)])
 def test_mixed_chunks_full(hq, hkv):
     b = make_batch_from_lens(MIXED_L, MIXED_N, dtype="bf16", num_q_heads=hq, num_kv_heads=hkv,
                              head_dim=128, block_size=16, seed=31)
