@@ -130,3 +130,48 @@ def test_mixed_step_chunk_plus_decode():
     drows = [r for r in rows if r >= 8192]
     assert_parity(f64(dec)[[r - 8192 for r in drows]], ref[[rows.index(r) for r in drows]],
                   "bf16", "mixed step, decode part")
+
+
+def test_reference_moves_mid_sequence():
+    """Scores that jump far above everything before them, late in the context
+    and inside the chunk: every query row carries a shared direction u, and the
+    keys at three positions are a * u with a growing, so each of those keys
+    outgrows the rows' reference by more than 2^8. The kernel must move the
+    reference, rescale O and the row sum, and redo the step's exponentials
+    (prefill), or rescale its running state (decode), and still match the
+    oracle. The keys are written into the layer by the oracle's own append."""
+    import oracle
+    import paper_2608_23658_amd.kvattn as K
+    L, n = 2500, 600
+    b = make_batch_from_lens([L], [n], dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=77)
+    g = torch.Generator().manual_seed(78)
+    u = torch.randn(128, generator=g)
+    u = u / u.norm()
+    b.q = (b.q.float() + 2.0 * 128 ** 0.5 * u).to(torch.bfloat16)
+    pos = np.array([900, 1700, 2400])
+    amp = [4.0, 8.0, 16.0]
+    k_new = torch.stack([a * u.expand(8, 128) for a in amp]).to(torch.bfloat16)
+    v_new = torch.randn(3, 8, 128, generator=g).to(torch.bfloat16)
+    slots = (b.block_table[0][pos // 16].astype(np.int64) * 16 + pos % 16).astype(np.int32)
+    u16 = lambda t: t.view(torch.int16).numpy().view(np.uint16)
+    raw = oracle.kv_append(b.kv_raw(), u16(k_new), u16(v_new), slots, dtype="bf16",
+                           num_kv_heads=8, head_dim=128, block_size=16)
+    b.kv_layer = torch.from_numpy(raw.view(np.int16)).view(torch.bfloat16)
+    say("prefill with late score jumps at", pos.tolist())
+    dev = Dev(b)
+    out = dev.prefill()
+    torch.cuda.synchronize()
+    ref = oracle_prefill(b)
+    # the rows at and after the last jump attend to it almost alone
+    assert np.abs(ref[pos[2] - (L - n):, 0] - f64(v_new[2, 0])).max() < 1e-3
+    assert_parity(out, ref, "bf16", "prefill with late score jumps", seq_bounds(b))
+    say("decode over the same layer")
+    qd = b.q[-1:].contiguous()
+    od = K.decode(qd.cuda(), dev.kv, b.num_blocks, dev.bt, dev.sl, num_kv_heads=8,
+                  max_seq_len=L, scale=b.scale)
+    torch.cuda.synchronize()
+    refd = oracle.paged_decode(u16(qd), raw, b.block_table, b.seq_lens, dtype="bf16",
+                               num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=16,
+                               scale=b.scale)
+    assert_parity(od, refd, "bf16", "decode with late score jumps")
