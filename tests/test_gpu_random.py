@@ -56,3 +56,25 @@ def test_prefill_random(seed):
     torch.cuda.synchronize()
     assert out.shape[0] == sum(n)
     assert_parity(out, oracle_prefill(b), "bf16", f"prefill random {seed}", seq_bounds(b))
+
+
+def test_many_short_sequences():
+    """Wide batches: 4096 decode sequences and 1024 prefill chunks of 1 to 64
+    tokens (the decode grid and the prefill work-tile list at many entries),
+    each sequence gated on its own."""
+    rng = np.random.default_rng(4096)
+    lens = [int(x) for x in rng.integers(1, 65, size=4096)]
+    say("decode, 4096 sequences")
+    b = make_batch_from_lens(lens, [1] * len(lens), dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=4097)
+    out = Dev(b).decode()
+    torch.cuda.synchronize()
+    assert_parity(out, oracle_decode(b), "bf16", "decode, 4096 sequences", seq_bounds(b, decode=True))
+    lens = [int(x) for x in rng.integers(1, 65, size=1024)]
+    n = [int(rng.integers(1, L + 1)) for L in lens]
+    say("prefill, 1024 chunks")
+    b = make_batch_from_lens(lens, n, dtype="bf16", num_q_heads=32, num_kv_heads=8,
+                             head_dim=128, block_size=16, seed=4098)
+    out = Dev(b).prefill()
+    torch.cuda.synchronize()
+    assert_parity(out, oracle_prefill(b), "bf16", "prefill, 1024 chunks", seq_bounds(b))
