@@ -24,7 +24,7 @@ ARCH = "gfx950"
 SOURCES = ["abi.cpp", "kvpool.cpp", "blockpool.cpp", "decode.hip", "prefill.hip", "append.hip",
            "blocks.hip"]
 
-COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-Werror=inline-asm",
           "-I", INCLUDE, "-I", CSRC]
 # Device code: gfx950 only; packed fp32 instructions disabled.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",

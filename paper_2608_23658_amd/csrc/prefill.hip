@@ -77,23 +77,55 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 
 constexpr uint32_t kBf16OnePair = 0x3f803f80u;   // (1.0, 1.0) in bf16
 
-// 16 bytes per lane from global memory straight into LDS: lane l reads
-// base + off_l and its bytes go to LDS byte address lds + 16 l (base and lds
-// must be wave-uniform). The address is given as a wave-uniform base in
-// SGPRs plus a 32-bit per-lane offset, which the memory pipeline takes in
-// fewer cycles per instruction than 64 lanes of 64-bit addresses. Issued as
-// inline assembly so that the compiler does not treat it as an LDS store
-// that every later LDS read must wait for: the callers wait for these loads
+// Two loads of 16 bytes per lane from global memory straight into LDS
+// (global_load_lds_dwordx4): load j has lane l read base_j + off_j and its
+// bytes land at LDS byte address lds_j + 16 l (base_j and lds_j wave-uniform,
+// in SGPRs). A wave-uniform base plus a 32-bit lane offset takes the address
+// unit fewer cycles per instruction than 64 lanes of 64-bit addresses. M0
+// carries each load's LDS address: the block saves the compiler's M0 first
+// and restores it last, so no code outside the block sees M0 change. Issued
+// as inline assembly so that the compiler does not treat the loads as LDS
+// stores that every later LDS read must wait for: the callers wait for them
 // themselves (s_waitcnt vmcnt) before the barrier that publishes the data.
-__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
+__device__ __forceinline__ void dma16x2(const void* base0, uint32_t off0, uint32_t lds0,
+                                        const void* base1, uint32_t off1, uint32_t lds1) {
+  uint32_t saved;
   asm volatile(
-      "s_mov_b32 m0, %2\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, %1"
-      :
-      : "v"(off), "s"(base), "s"(lds)
-      : "memory", "m0");
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %6\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %4, %5\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off0), "s"(base0), "s"(lds0), "v"(off1), "s"(base1), "s"(lds1)
+      : "memory");
 }
+
+// Entry i of a block-table row, read by a scalar memory load: the row pointer
+// is wave-uniform and the index is made so, and a load through the constant
+// address space from a uniform address is a scalar load. It is therefore
+// counted by lgkmcnt, never by the vmcnt that the gathers are waited with.
+__device__ __forceinline__ int scalar_entry(const int* row, int i) {
+  const __attribute__((address_space(4))) int* p =
+      (const __attribute__((address_space(4))) int*)row;
+  return p[(unsigned)__builtin_amdgcn_readfirstlane(i)];
+}
+
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef i32x4_t i32x4_a4_t __attribute__((aligned(4)));
+
+// Entries i .. i + 3 of a block-table row in one 16-byte scalar load (scalar
+// loads need only 4-byte alignment).
+__device__ __forceinline__ i32x4_t scalar_entries4(const int* row, int i) {
+  const __attribute__((address_space(4))) i32x4_a4_t* p =
+      (const __attribute__((address_space(4))) i32x4_a4_t*)(
+          row + (unsigned)__builtin_amdgcn_readfirstlane(i));
+  return *p;
+}
+
 // LDS byte address of a pointer into a __shared__ array.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
@@ -109,10 +141,21 @@ __device__ __forceinline__ int lane_id_fresh() {
 
 }  // namespace
 
+// Rows [lo, hi) of sequence s's chunk, with the offsets clamped into
+// [0, total_q] and hi >= lo, so that offsets that break the documented
+// contract (decreasing, or past the end of q) can neither read nor write
+// outside q and out.
+__device__ __forceinline__ int2 chunk_rows(const int* __restrict__ cu, int s, int total_q) {
+  const int lo = min(max(cu[s], 0), total_q);
+  const int hi = min(max(cu[s + 1], lo), total_q);
+  return make_int2(lo, hi);
+}
+
 // Lists the work tiles (sequence, first row) of a batch of chunks, the rows
 // of a sequence's chunk in descending order so the longest rows start first.
 __global__ __launch_bounds__(256) void prefill_tile_map_kernel(const int* __restrict__ cu,
-                                                               int num_seqs, int rows_per_tile,
+                                                               int num_seqs, int total_q,
+                                                               int rows_per_tile,
                                                                int2* __restrict__ tiles,
                                                                int* __restrict__ count,
                                                                int max_tiles) {
@@ -123,8 +166,8 @@ __global__ __launch_bounds__(256) void prefill_tile_map_kernel(const int* __rest
   const int s1 = min(num_seqs, s0 + per);
   int mine = 0;
   for (int s = s0; s < s1; ++s) {
-    const int n = max(0, cu[s + 1] - cu[s]);
-    mine += (n + rows_per_tile - 1) / rows_per_tile;
+    const int2 r = chunk_rows(cu, s, total_q);
+    mine += (r.y - r.x + rows_per_tile - 1) / rows_per_tile;
   }
   scan[tid] = mine;
   __syncthreads();
@@ -136,8 +179,8 @@ __global__ __launch_bounds__(256) void prefill_tile_map_kernel(const int* __rest
   }
   int off = scan[tid] - mine;
   for (int s = s0; s < s1; ++s) {
-    const int n = max(0, cu[s + 1] - cu[s]);
-    const int nt = (n + rows_per_tile - 1) / rows_per_tile;
+    const int2 r = chunk_rows(cu, s, total_q);
+    const int nt = (r.y - r.x + rows_per_tile - 1) / rows_per_tile;
     for (int k = 0; k < nt; ++k) {
       if (off < max_tiles) tiles[off] = make_int2(s, (nt - 1 - k) * rows_per_tile);
       ++off;
@@ -153,7 +196,8 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
                     int num_blocks, const int* __restrict__ block_table,
                     const int* __restrict__ seq_lens, const int* __restrict__ cu,
                     uint16_t* __restrict__ out, const int2* __restrict__ tiles,
-                    const int* __restrict__ tile_count, int num_q_heads, int num_kv_heads,
+                    const int* __restrict__ tile_count, int total_q, int num_q_heads,
+                    int num_kv_heads,
                     int max_blocks, int max_seq_len, float scale_log2) {
   constexpr int kRows = 32 * kWaves / G;   // rows per work tile
   const int wid = blockIdx.x;
@@ -168,8 +212,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   const int lane = tid % kWave;
   const int h = g * G + wave % G;
   const int row0 = q0 + (wave / G) * 32;        // first row of this wave
-  const int cu0 = cu[s];
-  const int n = cu[s + 1] - cu0;
+  const int2 rows = chunk_rows(cu, s, total_q);
+  const int cu0 = rows.x;
+  const int n = rows.y - rows.x;
   int L = seq_lens[s];
   L = __builtin_amdgcn_readfirstlane(min(max(L, 0), min(max_seq_len, max_blocks * kBS)));
   const int c = L - n;                          // cached context before the chunk
@@ -220,50 +265,79 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   float l_run = 0.f;         // lane-partial row sum
 
   // ---- gather of K or V of one 64-key step straight into LDS (global_load_lds) ----
-  // A half step is 4 tiles of 4 KiB (blocks 0..3); in round j wavefront w
-  // fills quarter (w + 8 j) % 4 of tile (w + 8 j) / 4, a contiguous 1 KiB with
-  // 16 bytes per lane. K is copied as stored; for V the lane picks the global
-  // 16 bytes that belong at its swizzled LDS position (row pos / 2, half
-  // pos % 2 holds global half (pos % 2) ^ ((row >> 3) & 1)). A block past L
-  // or with an id outside [0, num_blocks) is replaced by block 0 (the host
-  // guarantees one exists); the returned bit mask (bit kb: block kb is real)
-  // lets the softmax mask its keys and patch_v zero its values.
-  auto load_half = [&](auto v_tag, int step) __attribute__((always_inline)) {
-    constexpr bool kV = decltype(v_tag)::value;
-    const int kbase = step * kKeys;
-    // block id of block kb of the step, or -1 if it is not real
-    auto block_id = [&](int kb) __attribute__((always_inline)) {
-      const int key0 = kbase + kb * kBS;
-      const int id = key0 < L ? bt[key0 / kBS] : -1;
-      return (unsigned)id < (unsigned)num_blocks ? id : -1;
-    };
+  // The block ids of a step are read from the table first (step_ids), in
+  // SGPRs: one 16-byte scalar load when all 4 blocks lie inside the sequence,
+  // single entries otherwise; a block past L or with an id outside
+  // [0, num_blocks) gets id -1. The bit mask of a step (bit kb: block kb is
+  // real) lets the softmax mask its keys and patch_v zero its values.
+  const int nblk = (L + kBS - 1) / kBS;   // table entries the sequence uses
+  struct StepIds {
+    int id[kStepBlocks];
+  };
+  auto step_ids = [&](int step) __attribute__((always_inline)) {
+    StepIds r;
+    const int b0 = step * kStepBlocks;
+    if (b0 + kStepBlocks <= nblk) {
+      const i32x4_t v = scalar_entries4(bt, b0);
+#pragma unroll
+      for (int kb = 0; kb < kStepBlocks; ++kb) r.id[kb] = v[kb];
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < kStepBlocks; ++kb)
+        r.id[kb] = b0 + kb < nblk ? scalar_entry(bt, b0 + kb) : -1;
+    }
+    return r;
+  };
+  // Ids are checked against the layer only where they are used, so that
+  // nothing waits for the loads where they are issued.
+  auto real_id = [&](int id) __attribute__((always_inline)) {
+    return (unsigned)id < (unsigned)num_blocks;
+  };
+  auto id_bits = [&](const StepIds& r) __attribute__((always_inline)) {
     int bits = 0;
 #pragma unroll
-    for (int kb = 0; kb < kStepBlocks; ++kb) bits |= block_id(kb) >= 0 ? (1 << kb) : 0;
+    for (int kb = 0; kb < kStepBlocks; ++kb) bits |= real_id(r.id[kb]) ? (1 << kb) : 0;
+    return bits;
+  };
+  // The gather itself: a half step is 4 tiles of 4 KiB (blocks 0..3); in
+  // round j wavefront w fills quarter (w + 8 j) % 4 of tile (w + 8 j) / 4, a
+  // contiguous 1 KiB with 16 bytes per lane. K is copied as stored; for V the
+  // lane picks the global 16 bytes that belong at its swizzled LDS position
+  // (row pos / 2, half pos % 2 holds global half (pos % 2) ^ ((row >> 3) & 1)).
+  // A block that is not real is read from block 0 instead (the host
+  // guarantees one exists) and masked afterwards.
+  auto gather = [&](auto v_tag, int step, const StepIds& ids) __attribute__((always_inline)) {
+    constexpr bool kV = decltype(v_tag)::value;
     // The lane id is recomputed here rather than kept live across the step.
     const int ln = lane_id_fresh();
+    const uint8_t* base[2];
+    uint32_t off[2], lds[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int kb = (wave + kWaves * j) / 4;     // wave-uniform
       const int quarter = (wave + kWaves * j) % 4;
-      const int id = block_id(kb);
-      const size_t id0 = (size_t)(id >= 0 ? id : 0);
-      const uint8_t* base =
-          kv + (kPow2Blocks ? id0 << block_shift : id0 * block_bytes) + (kV ? v_off : k_off);
-      const int pos = quarter * kWave + ln;       // 16-byte position in the tile
+      // kb is wave / 4 + 2 j: pick the id by a uniform select, not an index
+      const int id = wave < 4 ? ids.id[2 * j] : ids.id[2 * j + 1];
+      const size_t id0 = real_id(id) ? (size_t)(unsigned)id : 0;
+      base[j] = kv + (kPow2Blocks ? id0 << block_shift : id0 * block_bytes) + (kV ? v_off : k_off);
+      const unsigned pos = quarter * kWave + (unsigned)ln;   // 16-byte position in the tile
       if constexpr (kV) {
-        const int vrow = pos / 2;
-        const int src = vrow * 32 + (((pos % 2) ^ ((vrow >> 3) & 1)) * 16);
-        dma16(base, (uint32_t)src,
-              __builtin_amdgcn_readfirstlane(
-                  lds_addr(&lds_v[step % kVBufs][kb][quarter * 1024])));
+        const unsigned vrow = pos / 2;
+        off[j] = vrow * 32 + (((pos % 2) ^ ((vrow >> 3) & 1)) * 16);
+        lds[j] = __builtin_amdgcn_readfirstlane(
+            lds_addr(&lds_v[step % kVBufs][kb][quarter * 1024]));
       } else {
-        dma16(base, (uint32_t)(pos * 16),
-              __builtin_amdgcn_readfirstlane(
-                  lds_addr(&lds_k[step % kKBufs][kb][quarter * 1024])));
+        off[j] = pos * 16;
+        lds[j] = __builtin_amdgcn_readfirstlane(
+            lds_addr(&lds_k[step % kKBufs][kb][quarter * 1024]));
       }
     }
-    return bits;
+    dma16x2(base[0], off[0], lds[0], base[1], off[1], lds[1]);
+  };
+  auto load_half = [&](auto v_tag, int step) __attribute__((always_inline)) {
+    const StepIds ids = step_ids(step);
+    gather(v_tag, step, ids);
+    return id_bits(ids);
   };
   // Zero the V slots of a landed step that must not contribute: blocks that
   // are not real, and slots at or past L (their bytes may be NaN, and a zero
@@ -273,9 +347,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   // only when such slots exist.
   auto patch_v = [&](int step, int bits) __attribute__((always_inline)) {
     const int kbase = step * kKeys;
+    // recomputed here, so no lane constant of this rare path stays live
+    // across the pipelined loop
+    const int ln = lane_id_fresh();
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      const int cidx = lane + kWave * j;          // 16-byte chunk of the 4 V tiles
+      const int cidx = ln + kWave * j;            // 16-byte chunk of the 4 V tiles
       const int kb = cidx / 256;
       const int pos = cidx % 256;
       const int vrow = pos / 2;
@@ -323,6 +400,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     }
   };
   // O^T += V^T P^T for one step: one k-step per block, 4 accumulator chains.
+  // Used once per tile, after the pipelined loop; the fence after each block
+  // keeps the compiler from hoisting all 16 operand reads at once, which
+  // would need more registers than the kernel has left.
   auto pv = [&](int step, const bf16x8_t (&pr)[4]) {
     const int buf = step % kVBufs;
 #pragma unroll
@@ -333,18 +413,20 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
             *reinterpret_cast<const bf16x8_t*>(&lds_v[buf][kb][dt * 32 * 32 + v_read]);
         oacc[dt] = mfma32(a, pr[kb], oacc[dt]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Causal / length / real-block mask of one step's scores, in place; run
   // only on the steps that need it.
   auto mask_scores = [&](int step, int bits, f32x16_t (&sr)[2]) {
     const int kbase = step * kKeys;
-    const int qpos = wave_pos0 + lm;
+    const int ln = lane_id_fresh();   // as in patch_v
+    const int qpos = wave_pos0 + ln % 32;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int kpos = kbase + kt * 32 + (i / 8) * 16 + lh * 8 + (i % 8);
+        const int kpos = kbase + kt * 32 + (i / 8) * 16 + (ln / 32) * 8 + (i % 8);
         const int blk_ok = (bits >> (2 * kt + i / 8)) & 1;
         const int keep = (kpos <= qpos) & (kpos < L) & blk_ok;
         sr[kt][i] = keep ? sr[kt][i] : -INFINITY;
@@ -355,6 +437,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
   };
   // bitsm1, bits0 .. bits3: real-block masks of steps i - 1, i .. i + 3
   int bitsm1 = 0, bits0 = 0, bits1 = 0, bits2 = 0, bits3 = 0;
+  // block ids of the gathers of the coming phase: K of step i + 3 and V of
+  // step i + 1, read at the end of the phase before (ahead of its barrier)
+  StepIds idsK, idsV;
   f32x16_t sA[2], sB[2];    // scores of even / odd steps
   bf16x8_t pA[4], pB[4];    // P of even / odd steps
 
@@ -381,6 +466,12 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
                    f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4], bf16x8_t (&p_cur)[4]) __attribute__((always_inline)) {
     constexpr bool kQK = decltype(qk_tag)::value;
     constexpr bool kPV = decltype(pv_tag)::value;
+    // The block ids were read before the barrier that ends the previous
+    // phase: wait for them here, while no operand read of this phase is in
+    // flight, so that the operand prefetch below is never drained for them
+    // (scalar loads share the lgkm counter with LDS reads and return out of
+    // order).
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
     if (kPV && !step_clean(i - 1, bitsm1)) patch_v(i - 1, bitsm1);
     const bool do_k = i + 3 < N, do_v = i + 1 < N;
     if (needs_mask(i, bits0)) mask_scores(i, bits0, s_cur);
@@ -396,7 +487,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       return *reinterpret_cast<const bf16x8_t*>(
           &lds_k[kbuf][2 * kt + k_blk][((2 * ks + lh) * kBS + k_slot) * 16]);
     };
-    constexpr int kAhead = 5;
+    constexpr int kAhead = kQK ? 5 : 3;   // the last step keeps fewer reads in flight
     bf16x8_t fr[kAhead + 1];
 #pragma unroll
     for (int k = 0; k < kAhead; ++k) {
@@ -434,8 +525,11 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       }
       // the step's gathers, issued inside the schedule (K in slot 10, V in
       // slot 26) so that their LDS writes do not land in one burst
-      if (k == 10 && do_k) bits3 = load_half(std::false_type{}, i + 3);
-      if (k == 26 && do_v) load_half(std::true_type{}, i + 1);
+      if (k == 10 && do_k) {
+        gather(std::false_type{}, i + 3, idsK);
+        bits3 = id_bits(idsK);
+      }
+      if (k == 26 && do_v) gather(std::true_type{}, i + 1, idsV);
       __builtin_amdgcn_sched_barrier(0);
     }
     // A row without a reference yet, or a lane whose partial row sum (which
@@ -477,6 +571,9 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
 #pragma unroll
     for (int k = 0; k < 4; ++k) asm volatile("" ::"v"(p_cur[k]));
     asm volatile("" ::"v"(l_run));
+    // the block ids of the next phase's gathers
+    if (i + 4 < N) idsK = step_ids(i + 4);
+    if (i + 2 < N) idsV = step_ids(i + 2);
     // wait for the gathers of steps before this one (each thread issued two
     // for K when i + 3 < N and two for V when i + 1 < N in this step)
     if (i + 3 < N)
@@ -529,6 +626,8 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     if (N > 1) bits1 = load_half(std::false_type{}, 1);
     if (N > 2) bits2 = load_half(std::false_type{}, 2);
     load_half(std::true_type{}, 0);
+    if (N > 3) idsK = step_ids(3);
+    if (N > 1) idsV = step_ids(1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     qk(0, sA);
@@ -591,7 +690,7 @@ static hipError_t launch_prefill_t(const PrefillArgs& a) {
   const int grid_tiles = (int)(bound < max_tiles ? bound : max_tiles);
   trace_before(a.stream, "prefill_tile_map");
   hipLaunchKernelGGL(prefill_tile_map_kernel, dim3(1), dim3(256), 0, a.stream, a.cu_seqlens_q,
-                     a.num_seqs, kRowsPerTile, tiles, count, grid_tiles);
+                     a.num_seqs, a.total_q_tokens, kRowsPerTile, tiles, count, grid_tiles);
   trace_after(a.stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -604,8 +703,9 @@ static hipError_t launch_prefill_t(const PrefillArgs& a) {
   hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), 0, a.stream,
                      static_cast<const uint16_t*>(a.q), static_cast<const uint8_t*>(a.kv),
                      a.num_blocks, a.block_table, a.seq_lens, a.cu_seqlens_q,
-                     static_cast<uint16_t*>(a.out), tiles, count, a.num_q_heads,
-                     a.num_kv_heads, a.max_blocks, a.max_seq_len, a.scale * kLog2e);
+                     static_cast<uint16_t*>(a.out), tiles, count, a.total_q_tokens,
+                     a.num_q_heads, a.num_kv_heads, a.max_blocks, a.max_seq_len,
+                     a.scale * kLog2e);
   trace_after(a.stream);
   return hipGetLastError();
 }

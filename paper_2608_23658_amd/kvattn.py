@@ -159,6 +159,18 @@ def _require_int32(**named):
         raise ValueError("block_table must be [num_seqs, max_blocks_per_seq]")
 
 
+def _require_rows(num_seqs: int, block_table, seq_lens, cu_seqlens_q=None):
+    """The per-sequence tensors reach the kernels as bare pointers: their
+    lengths must match the batch, or the kernels would read past them."""
+    if tuple(seq_lens.shape) != (num_seqs,):
+        raise ValueError(f"seq_lens must be [{num_seqs}], not {tuple(seq_lens.shape)}")
+    if block_table.shape[0] != num_seqs:
+        raise ValueError(f"block_table must have {num_seqs} rows, not {block_table.shape[0]}")
+    if cu_seqlens_q is not None and tuple(cu_seqlens_q.shape) != (num_seqs + 1,):
+        raise ValueError(f"cu_seqlens_q must be [{num_seqs + 1}], "
+                         f"not {tuple(cu_seqlens_q.shape)}")
+
+
 def _require_out(out, q):
     if out is not None and (out.dtype != q.dtype or out.shape != q.shape):
         raise ValueError("out must have q's shape and dtype")
@@ -180,6 +192,7 @@ def decode_two_tensor(q: torch.Tensor, kv_base, num_base: int, kv_elastic, num_e
     """Decode over a layer split into two tensors (ids >= num_base in the second)."""
     B, Hq, d = q.shape
     _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_rows(B, block_table, seq_lens)
     _require_out(out, q)
     _require_cuda(q, kv_base, kv_elastic, block_table, seq_lens, out, ws)
     if out is None:
@@ -219,6 +232,7 @@ def decode(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor
     """
     B, Hq, d = q.shape
     _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_rows(B, block_table, seq_lens)
     _require_out(out, q)
     _require_cuda(q, kv_layer, block_table, seq_lens, out, ws)
     if out is None:
@@ -244,9 +258,10 @@ def prefill_chunk(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch
     """Chunked prefill: ``q`` [T, Hq, d] bf16, chunks given by ``cu_seqlens_q``."""
     T, Hq, d = q.shape
     _require_int32(block_table=block_table, seq_lens=seq_lens, cu_seqlens_q=cu_seqlens_q)
+    B = int(seq_lens.shape[0])
+    _require_rows(B, block_table, seq_lens, cu_seqlens_q)
     _require_out(out, q)
     _require_cuda(q, kv_layer, block_table, seq_lens, cu_seqlens_q, out, ws)
-    B = int(seq_lens.shape[0])
     if out is None:
         out = torch.empty_like(q)
     if ws is None:

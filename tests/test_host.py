@@ -269,8 +269,9 @@ def test_binding_rejects_views_and_wide_indices_before_any_launch():
     sl = torch.ones(4, dtype=torch.int32)
     with pytest.raises(ValueError, match="int32"):
         K.decode(q, 0, 10, bt.long(), sl, num_kv_heads=2, max_seq_len=48)
+    strided = torch.zeros(4, 8, 256, dtype=torch.bfloat16)[:, :, :128]
     with pytest.raises(ValueError, match="contiguous"):
-        K.decode(q.transpose(0, 1), 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48)
+        K.decode(strided, 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48)
     with pytest.raises(ValueError, match="block_table"):
         K.decode(q, 0, 10, bt.flatten(), sl, num_kv_heads=2, max_seq_len=48)
     with pytest.raises(ValueError, match="out"):
@@ -280,3 +281,25 @@ def test_binding_rejects_views_and_wide_indices_before_any_launch():
         K.prefill_chunk(q, 0, 10, bt, sl, cu, num_kv_heads=2, max_seq_len=48)
     with pytest.raises(ValueError, match="GPU"):
         K.decode(q, 0, 10, bt, sl, num_kv_heads=2, max_seq_len=48)
+
+
+def test_binding_checks_batch_lengths_before_any_launch():
+    """seq_lens, the block-table rows and cu_seqlens_q reach the kernels as
+    bare pointers indexed by sequence: lengths that do not match the batch
+    would make them read past the tensors, so the binding refuses them."""
+    import torch
+    q = torch.zeros(4, 8, 128, dtype=torch.bfloat16)
+    bt = torch.zeros(4, 3, dtype=torch.int32)
+    sl = torch.ones(4, dtype=torch.int32)
+    with pytest.raises(ValueError, match="seq_lens"):
+        K.decode(q, 0, 10, bt, sl[:3], num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="block_table"):
+        K.decode(q, 0, 10, bt[:3], sl, num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="seq_lens"):
+        K.decode_two_tensor(q, 0, 5, 0, 5, bt, sl[:2], num_kv_heads=2, max_seq_len=48)
+    # prefill: 2 sequences over 4 new rows
+    cu = torch.tensor([0, 2, 4], dtype=torch.int32)
+    with pytest.raises(ValueError, match="cu_seqlens_q"):
+        K.prefill_chunk(q, 0, 10, bt[:2], sl[:2], cu[:2], num_kv_heads=2, max_seq_len=48)
+    with pytest.raises(ValueError, match="block_table"):
+        K.prefill_chunk(q, 0, 10, bt, sl[:2], cu, num_kv_heads=2, max_seq_len=48)
