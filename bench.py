@@ -14,7 +14,6 @@ from __future__ import annotations
 import argparse
 import json
 import os
-import resource
 import statistics
 import sys
 import time
@@ -499,40 +498,93 @@ def elastic_leg(args, K, work):
     return res
 
 
-def cpu_baseline(b, work, seconds):
-    """The fp64 oracle on the first sequences of the decode batch, as many as
-    fit in about `seconds` of wall time; reported in the headline's unit."""
-    import oracle
-    seqs, t0 = [], time.perf_counter()
-    r0 = resource.getrusage(resource.RUSAGE_SELF)
-    for s in range(b.num_seqs):
-        oracle.paged_decode(b.q_raw(), b.kv_raw(), b.block_table, b.seq_lens, dtype=b.dtype,
-                            num_q_heads=b.num_q_heads, num_kv_heads=b.num_kv_heads,
-                            head_dim=b.head_dim, block_size=b.block_size, scale=b.scale,
-                            seqs=[s])
-        seqs.append(s)
-        if time.perf_counter() - t0 > seconds:
-            break
-    wall = time.perf_counter() - t0
-    r1 = resource.getrusage(resource.RUSAGE_SELF)
-    cpu = (r1.ru_utime - r0.ru_utime) + (r1.ru_stime - r0.ru_stime)
-    lens = b.seq_lens[seqs]
-    nbytes = work.decode_bytes(lens, b.num_q_heads, b.num_kv_heads, b.head_dim, b.esz)
-    model = ""
+def _cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
             for ln in f:
                 if ln.startswith("model name"):
-                    model = ln.split(":", 1)[1].strip()
-                    break
+                    return ln.split(":", 1)[1].strip()
     except OSError:
         pass
-    return {"value": round(nbytes / wall / 1e9, 4), "unit": "GB/s",
-            "cores": round(cpu / wall, 2), "kind": "oracle",
-            "sample": f"fp64 oracle decode of the first {len(seqs)} of {b.num_seqs} sequences "
-                      f"({int(lens.sum())} context tokens, {nbytes} algorithmic bytes) in "
-                      f"{wall:.1f} s wall, {cpu:.1f} s CPU",
-            "cpu_model": model, "threads_available": len(os.sched_getaffinity(0))}
+    return ""
+
+
+def cpu_baseline(dec_batch, work, seconds):
+    """The fp64 oracle, as it stands, on the host cores of this process:
+    n = the CPUs this process may run on, and every thread pool the oracle
+    can use (numpy's BLAS, torch) is set to n. Timed on bounded samples:
+
+    - the decode workload (256 sequences, lengths U[512, 4096]): whole
+      sequences in order until about `seconds` of wall time have passed,
+      reported in the headline's unit (algorithmic GB/s);
+    - the tiny fp32 decode, in full;
+    - the mixed step's prefill chunk (8192 rows over 24576 cached tokens):
+      four 256-row tiles at the chunk's start, one third, two thirds and end,
+      each as the chunk of a sequence that ends at the tile's last row (a
+      row's result depends only on the keys up to it), in algorithmic
+      TFLOP/s of the sampled rows."""
+    import threadpoolctl
+
+    import oracle
+    from workloads import MIXED_STEP, TINY_DECODE_F32, make_batch
+
+    n = len(os.sched_getaffinity(0))
+    torch.set_num_threads(n)
+    res = {}
+    with threadpoolctl.threadpool_limits(limits=n):
+        def decode_rate(b, budget):
+            seqs, t0 = [], time.perf_counter()
+            for s in range(b.num_seqs):
+                oracle.paged_decode(b.q_raw(), b.kv_raw(), b.block_table, b.seq_lens,
+                                    dtype=b.dtype, num_q_heads=b.num_q_heads,
+                                    num_kv_heads=b.num_kv_heads, head_dim=b.head_dim,
+                                    block_size=b.block_size, scale=b.scale, seqs=[s])
+                seqs.append(s)
+                if time.perf_counter() - t0 > budget:
+                    break
+            wall = time.perf_counter() - t0
+            lens = b.seq_lens[seqs]
+            nbytes = work.decode_bytes(lens, b.num_q_heads, b.num_kv_heads, b.head_dim, b.esz)
+            return nbytes, wall, len(seqs), int(lens.sum())
+
+        nbytes, wall, ns, ntok = decode_rate(dec_batch, seconds)
+        head = {"value": round(nbytes / wall / 1e9, 4), "unit": "GB/s", "cores": n,
+                "kind": "oracle",
+                "sample": f"fp64 oracle decode of the first {ns} of {dec_batch.num_seqs} "
+                          f"sequences of decode_b256_l512_4096_bf16 ({ntok} context tokens, "
+                          f"{nbytes} algorithmic bytes) in {wall:.2f} s wall on {n} threads",
+                "cpu_model": _cpu_model()}
+        res["decode_b256_l512_4096_bf16"] = {"value": head["value"], "unit": "GB/s",
+                                             "seconds": round(wall, 3), "sequences": ns}
+        tiny = make_batch(TINY_DECODE_F32)
+        nbytes, wall, ns, ntok = decode_rate(tiny, 60.0)
+        res[TINY_DECODE_F32.name] = {"value": round(nbytes / wall / 1e9, 6), "unit": "GB/s",
+                                     "seconds": round(wall, 4), "sequences": ns,
+                                     "sample": "in full"}
+        mb = make_batch(MIXED_STEP)
+        L, nq = int(mb.seq_lens[0]), int(mb.q_lens[0])
+        c = L - nq
+        T = mb.total_q_tokens
+        q_all = np.asarray(mb.q_raw()).reshape(T, mb.num_q_heads, mb.head_dim)
+        flops, t0 = 0, time.perf_counter()
+        tiles = [0, (nq // 3) // 256 * 256, (2 * nq // 3) // 256 * 256, nq - 256]
+        for r0 in tiles:
+            r1 = r0 + 256
+            oracle.paged_attention(q_all[r0:r1], mb.kv_raw(), mb.block_table[:1],
+                                   np.array([c + r1], dtype=np.int32),
+                                   np.array([0, r1 - r0], dtype=np.int32), dtype=mb.dtype,
+                                   num_q_heads=mb.num_q_heads, num_kv_heads=mb.num_kv_heads,
+                                   head_dim=mb.head_dim, block_size=mb.block_size,
+                                   scale=mb.scale)
+            flops += work.prefill_flops([c + r1], [r1 - r0], mb.num_q_heads, mb.head_dim)
+        wall = time.perf_counter() - t0
+        res["mixed_step_prefill_chunk8192_ctx24576"] = {
+            "value": round(flops / wall / 1e12, 6), "unit": "TFLOP/s",
+            "seconds": round(wall, 3),
+            "sample": f"rows {tiles} (+256 each) of the 8192-row chunk, {flops} algorithmic "
+                      f"FLOP; sampled, not the whole chunk"}
+    head["by_workload"] = res
+    return head
 
 
 def main():
@@ -574,9 +626,18 @@ def main():
         line["two_tensor_decode"] = two_tensor_leg(args, K, work, dec_batch)
     if args.workload in ("all", "prefill"):
         pre, _ = prefill_leg(args, K, work)
-        line["prefill"] = pre
+        # the metric's second half as a flat record (the last 8192-token chunk
+        # over 24576 cached tokens), with both cases nested under it
+        p = pre["chunk8192_ctx24576"]
+        line["prefill"] = {
+            "metric": "chunked-prefill attn TFLOP/s (% bf16 MFMA peak)",
+            "value": round(p["tflops"], 2), "unit": "TFLOP/s",
+            "ms_per_step": round(p["ms_per_call"], 5), "dtype": "bf16",
+            "config": {"workload": "prefill_chunk8192_ctx24576_bf16", "new_tokens": 8192,
+                       "cached_tokens": 24576, "num_q_heads": 32, "num_kv_heads": 8,
+                       "head_dim": 128, "block_size": 16},
+            "roofline": p["roofline"], "cases": pre}
         if line["value"] is None:
-            p = pre["chunk8192_ctx24576"]
             line.update(value=round(p["tflops"], 2), unit="TFLOP/s",
                         ms_per_step=round(p["ms_per_call"], 5), roofline=p["roofline"],
                         config={"workload": "prefill_chunk8192_ctx24576_bf16"})
