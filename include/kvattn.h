@@ -100,6 +100,32 @@ int kvattn_decode(const void* q, const void* kv_layer, int num_blocks,
                   int block_size, int max_blocks_per_seq, int max_seq_len, float scale,
                   kv_dtype dtype, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * decode as kvattn_decode, same arguments minus the workspace, and the same
+ * kernels and results. The split-K partials go to a fixed device array inside
+ * the library instead of a caller workspace:
+ *   - its size is kvattn_decode_noalloc_max_scratch_bytes() (32 MiB); a batch
+ *     whose partials need more (kvattn_decode_workspace_bytes(...) above that)
+ *     is refused with KV_ERR_INVALID before anything is launched (256
+ *     sequences of 32 query heads, head_dim 128, up to 4096 tokens, fit);
+ *   - each GPU the library runs on holds its own copy from its first call on
+ *     that GPU until the process ends; the array's device address is looked
+ *     up (hipGetSymbolAddress) on that first call, with the current device
+ *     being the one the stream belongs to;
+ *   - it allocates nothing and needs no initial contents, but every call on a
+ *     GPU shares that GPU's array: calls that overlap in time on one GPU
+ *     (different streams, or host threads) race and give undefined results.
+ *     Calls on one stream are ordered and safe.
+ * Errors as for kvattn_decode; KV_ERR_HIP if the array's address cannot be
+ * found. Asynchronous. */
+size_t kvattn_decode_noalloc_max_scratch_bytes(void);
+int kvattn_decode_noalloc(const void* q, const void* kv_layer, int num_blocks,
+                          const int32_t* block_table, const int32_t* seq_lens, void* out,
+                          int num_seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                          int block_size, int max_blocks_per_seq, int max_seq_len, float scale,
+                          kv_dtype dtype, void* stream);
+
 /* The rejected alternative (Section 3, "The contiguity constraint": split the
  * KV into two tensors and make the kernel read both). Same as kvattn_decode
  * but block ids below num_base_blocks address kv_base and ids from

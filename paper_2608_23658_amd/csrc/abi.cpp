@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -140,12 +141,32 @@ extern "C" size_t kvattn_decode_workspace_bytes(int num_seqs, int num_q_heads, i
 
 namespace {
 
+// Checks a decode call and fills the launch descriptor; the workspace is
+// checked only when check_workspace is set.
+int decode_check(const char* fn, const void* q, const void* kv_layer, const void* kv2,
+                 int num_base, int num_blocks, const int32_t* block_table,
+                 const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
+                 int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
+                 int max_seq_len, float scale, kv_dtype dtype, void* workspace,
+                 size_t workspace_bytes, bool check_workspace, void* stream,
+                 kvattn::DecodeArgs* a);
+
+int decode_launch(const char* fn, const kvattn::DecodeArgs& a);
+
 int decode_common(const char* fn, const void* q, const void* kv_layer, const void* kv2,
                   int num_base, int num_blocks, const int32_t* block_table,
                   const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
                   int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
                   int max_seq_len, float scale, kv_dtype dtype, void* workspace,
-                  size_t workspace_bytes, void* stream);
+                  size_t workspace_bytes, void* stream) {
+  kvattn::DecodeArgs a;
+  const int rc = decode_check(fn, q, kv_layer, kv2, num_base, num_blocks, block_table, seq_lens,
+                              out, num_seqs, num_q_heads, num_kv_heads, head_dim, block_size,
+                              max_blocks_per_seq, max_seq_len, scale, dtype, workspace,
+                              workspace_bytes, true, stream, &a);
+  if (rc != KV_OK || num_seqs == 0) return rc;
+  return decode_launch(fn, a);
+}
 
 }  // namespace
 
@@ -190,12 +211,13 @@ extern "C" int kvattn_decode_two_tensor(const void* q, const void* kv_base, int 
 
 namespace {
 
-int decode_common(const char* fn, const void* q, const void* kv_layer, const void* kv2,
-                  int num_base, int num_blocks, const int32_t* block_table,
-                  const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
-                  int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
-                  int max_seq_len, float scale, kv_dtype dtype, void* workspace,
-                  size_t workspace_bytes, void* stream) {
+int decode_check(const char* fn, const void* q, const void* kv_layer, const void* kv2,
+                 int num_base, int num_blocks, const int32_t* block_table,
+                 const int32_t* seq_lens, void* out, int num_seqs, int num_q_heads,
+                 int num_kv_heads, int head_dim, int block_size, int max_blocks_per_seq,
+                 int max_seq_len, float scale, kv_dtype dtype, void* workspace,
+                 size_t workspace_bytes, bool check_workspace, void* stream,
+                 kvattn::DecodeArgs* out_args) {
   if (num_seqs < 0) return set_error(KV_ERR_INVALID, "%s: num_seqs %d < 0", fn, num_seqs);
   if (dtype != KV_F32 && dtype != KV_BF16)
     return set_error(KV_ERR_INVALID, "%s: unknown dtype %d", fn, (int)dtype);
@@ -220,18 +242,21 @@ int decode_common(const char* fn, const void* q, const void* kv_layer, const voi
   if (num_kv_heads > 65535 || num_seqs > 65535)
     return set_error(KV_ERR_UNSUPPORTED, "%s: grid too large", fn);
   if (num_seqs == 0) return KV_OK;
-  if (!q || !kv_layer || !block_table || !seq_lens || !out || !workspace)
+  if (!q || !kv_layer || !block_table || !seq_lens || !out)
     return set_error(KV_ERR_INVALID, "%s: null pointer argument", fn);
-  if (!aligned16(q) || !aligned16(kv_layer) || !aligned16(out) || !aligned16(workspace))
-    return set_error(KV_ERR_INVALID, "%s: q, kv_layer, out and workspace must be "
-                                     "16-byte aligned", fn);
+  if (!aligned16(q) || !aligned16(kv_layer) || !aligned16(out))
+    return set_error(KV_ERR_INVALID, "%s: q, kv_layer and out must be 16-byte aligned", fn);
   DecodeWs w;
   decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w);
-  if (workspace_bytes < w.total)
-    return set_error(KV_ERR_INVALID, "%s: workspace %zu bytes < %zu needed", fn,
-                     workspace_bytes, w.total);
-
-  kvattn::DecodeArgs a;
+  if (check_workspace) {
+    if (!workspace) return set_error(KV_ERR_INVALID, "%s: null workspace", fn);
+    if (!aligned16(workspace))
+      return set_error(KV_ERR_INVALID, "%s: workspace must be 16-byte aligned", fn);
+    if (workspace_bytes < w.total)
+      return set_error(KV_ERR_INVALID, "%s: workspace %zu bytes < %zu needed", fn,
+                       workspace_bytes, w.total);
+  }
+  kvattn::DecodeArgs& a = *out_args;
   a.q = q;
   a.kv = kv_layer;
   a.num_blocks = num_blocks;
@@ -252,6 +277,10 @@ int decode_common(const char* fn, const void* q, const void* kv_layer, const voi
   a.stream = static_cast<hipStream_t>(stream);
   a.kv2 = kv2;
   a.num_base = num_base;
+  return KV_OK;
+}
+
+int decode_launch(const char* fn, const kvattn::DecodeArgs& a) {
   const hipError_t e = kvattn::launch_decode(a);
   if (e == hipErrorNotSupported) return set_error(KV_ERR_UNSUPPORTED, "%s: not built", fn);
   return hip_status(e, fn);
@@ -419,4 +448,77 @@ extern "C" int kvattn_copy_blocks(void* const* layers, int num_layers, int num_b
   a.dst = dst_ids;
   a.stream = static_cast<hipStream_t>(stream);
   return hip_status(kvattn::launch_copy_blocks(a), "kvattn_copy_blocks launch");
+}
+
+// ---------------------------------------------------------------------------
+// Decode without a caller workspace, for callers that cannot allocate device
+// memory (code under HIP graph capture, tight serving loops). The split-K
+// partials live in a file-scope device array of fixed size instead. Each GPU
+// the library runs on holds its own copy of the array, at its own address,
+// until the process ends. In host code the array's name is only a host-side
+// stand-in, so the device address is looked up once per device with
+// hipGetSymbolAddress and only that address is passed to the kernels.
+
+namespace {
+
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+
+__device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up with
+// that device current on the first call on it and kept for later calls.
+int scratch_on_current_device(const char* fn, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, fn);
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(KV_ERR_UNSUPPORTED, "%s: device %d beyond the %d the library tracks", fn,
+                     dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, fn);
+    if (!ptr) return set_error(KV_ERR_HIP, "%s: hipGetSymbolAddress gave no address", fn);
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return KV_OK;
+}
+
+}  // namespace
+
+extern "C" size_t kvattn_decode_noalloc_max_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+extern "C" int kvattn_decode_noalloc(const void* q, const void* kv_layer, int num_blocks,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     void* out, int num_seqs, int num_q_heads, int num_kv_heads,
+                                     int head_dim, int block_size, int max_blocks_per_seq,
+                                     int max_seq_len, float scale, kv_dtype dtype,
+                                     void* stream) {
+  clear_error();
+  const char* fn = "kvattn_decode_noalloc";
+  DecodeWs w;
+  if (!decode_ws(num_seqs, num_q_heads, head_dim, max_seq_len, &w))
+    return set_error(KV_ERR_INVALID, "%s: %d sequences, %d query heads, head_dim %d, "
+                                     "max_seq_len %d", fn, num_seqs, num_q_heads, head_dim,
+                     max_seq_len);
+  if (w.total > kNoAllocScratchBytes)
+    return set_error(KV_ERR_INVALID,
+                     "%s: the batch needs %zu bytes of split partials, more than the %zu-byte "
+                     "static scratch; use kvattn_decode with a workspace", fn, w.total,
+                     kNoAllocScratchBytes);
+  kvattn::DecodeArgs a;
+  int rc = decode_check(fn, q, kv_layer, nullptr, 0, num_blocks, block_table, seq_lens, out,
+                        num_seqs, num_q_heads, num_kv_heads, head_dim, block_size,
+                        max_blocks_per_seq, max_seq_len, scale, dtype, nullptr, 0, false,
+                        stream, &a);
+  if (rc != KV_OK || num_seqs == 0) return rc;
+  rc = scratch_on_current_device(fn, &a.workspace);
+  if (rc != KV_OK) return rc;
+  return decode_launch(fn, a);
 }

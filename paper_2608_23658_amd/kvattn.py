@@ -57,6 +57,9 @@ def lib() -> ctypes.CDLL:
     _c(L.kvattn_decode_split_tokens, i32, i32)
     _c(L.kvattn_decode, i32, vp, vp, i32, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
        i32, vp, sz, vp)
+    _c(L.kvattn_decode_noalloc_max_scratch_bytes, sz)
+    _c(L.kvattn_decode_noalloc, i32, vp, vp, i32, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
+       f32, i32, vp)
     _c(L.kvattn_decode_two_tensor, i32, vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, i32, i32,
        i32, i32, i32, f32, i32, vp, sz, vp)
     _c(L.kvattn_prefill_workspace_bytes, sz, i32, i32, i32, i32)
@@ -245,6 +248,33 @@ def decode(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor
                              int(block_size), int(block_table.shape[1]), int(max_seq_len),
                              float(scale), _dtype_code(q.dtype), _ptr(ws), ws.numel(),
                              _stream(stream))
+    check(rc)
+    return out
+
+
+def decode_noalloc_max_scratch_bytes() -> int:
+    return int(lib().kvattn_decode_noalloc_max_scratch_bytes())
+
+
+def decode_noalloc(q: torch.Tensor, kv_layer, num_blocks: int, block_table: torch.Tensor,
+                   seq_lens: torch.Tensor, out: torch.Tensor, *, num_kv_heads: int,
+                   max_seq_len: int, block_size: int = 16, scale: Optional[float] = None,
+                   stream=None) -> torch.Tensor:
+    """Paged decode through ``kvattn_decode_noalloc``: no workspace, and the
+    caller passes ``out`` so that nothing is allocated by the call."""
+    B, Hq, d = q.shape
+    _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_rows(B, block_table, seq_lens)
+    if out is None:
+        raise ValueError("decode_noalloc needs a caller-provided out")
+    _require_out(out, q)
+    _require_cuda(q, kv_layer, block_table, seq_lens, out)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    rc = lib().kvattn_decode_noalloc(_ptr(q), _ptr(kv_layer), int(num_blocks), _ptr(block_table),
+                                     _ptr(seq_lens), _ptr(out), B, Hq, int(num_kv_heads), d,
+                                     int(block_size), int(block_table.shape[1]),
+                                     int(max_seq_len), float(scale), _dtype_code(q.dtype),
+                                     _stream(stream))
     check(rc)
     return out
 

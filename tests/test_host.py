@@ -297,9 +297,32 @@ def test_binding_checks_batch_lengths_before_any_launch():
         K.decode(q, 0, 10, bt[:3], sl, num_kv_heads=2, max_seq_len=48)
     with pytest.raises(ValueError, match="seq_lens"):
         K.decode_two_tensor(q, 0, 5, 0, 5, bt, sl[:2], num_kv_heads=2, max_seq_len=48)
+    out = torch.empty_like(q)
+    with pytest.raises(ValueError, match="block_table"):
+        K.decode_noalloc(q, 0, 10, bt[:2], sl, out, num_kv_heads=2, max_seq_len=48)
     # prefill: 2 sequences over 4 new rows
     cu = torch.tensor([0, 2, 4], dtype=torch.int32)
     with pytest.raises(ValueError, match="cu_seqlens_q"):
         K.prefill_chunk(q, 0, 10, bt[:2], sl[:2], cu[:2], num_kv_heads=2, max_seq_len=48)
     with pytest.raises(ValueError, match="block_table"):
         K.prefill_chunk(q, 0, 10, bt, sl[:2], cu, num_kv_heads=2, max_seq_len=48)
+
+
+def test_noalloc_decode_refuses_before_touching_a_device(L):
+    """The allocation-free decode checks its sizes against its static scratch
+    (and the rest of its arguments) on the host, before any HIP call."""
+    cap = L.kvattn_decode_noalloc_max_scratch_bytes()
+    assert cap == 32 << 20
+
+    def call(**kw):
+        a = dict(B=256, hq=32, hkv=8, d=128, mb=4096, msl=4096 * 16, dt=K.KV_BF16)
+        a.update(kw)
+        return L.kvattn_decode_noalloc(A, A, 100, A, A, A, a["B"], a["hq"], a["hkv"], a["d"], 16,
+                                       a["mb"], a["msl"], 0.1, a["dt"], None)
+    assert call() == K.KV_ERR_INVALID                   # 64 splits of 256 x 32 rows: too big
+    assert "static scratch" in K.last_error()
+    assert K.decode_workspace_bytes(256, 32, 128, 4096 * 16) > cap
+    assert call(d=96, msl=160, mb=10) == K.KV_ERR_UNSUPPORTED
+    assert call(hq=30, msl=160, mb=10) == K.KV_ERR_INVALID
+    assert call(B=-1) == K.KV_ERR_INVALID
+    assert call(B=0, msl=160, mb=10) == K.KV_OK          # nothing to do
