@@ -260,9 +260,46 @@ int kvpool_sizes(const kvpool* pool, int* num_layers, size_t* base_bytes_per_lay
 
 /* Host wall-time breakdown of the last commit (create, map, set access) and
  * of the last decommit (device sync, unmap + release), in milliseconds.
- * Any output pointer may be NULL. */
+ * Any output pointer may be NULL. kvpool_last_toggle_steps below has every
+ * step on its own. */
 int kvpool_last_toggle_breakdown(const kvpool* pool, double* create_ms, double* map_ms,
                                  double* access_ms, double* sync_ms, double* unmap_ms);
+
+/* Host wall time of each step of the pool's last commit and last decommit,
+ * in milliseconds (steps a path does not take read 0). */
+typedef struct {
+  double commit_create_ms;     /* physical handles created */
+  double commit_copy_ms;       /* base contents copied into new handles (whole-handle) */
+  double commit_map_ms;        /* handles mapped into the layer ranges (whole-handle:
+                                  with the base handles unmapped first) */
+  double commit_access_ms;     /* read/write access granted */
+  double commit_release_ms;    /* base handles released (whole-handle) */
+  double decommit_sync_ms;     /* device synchronised */
+  double decommit_create_ms;   /* base handles created (whole-handle) */
+  double decommit_copy_ms;     /* base contents copied out (whole-handle) */
+  double decommit_unmap_ms;    /* elastic (whole-handle: whole) mappings removed */
+  double decommit_map_ms;      /* base handles mapped back (whole-handle) */
+  double decommit_access_ms;   /* access granted on the base (whole-handle) */
+  double decommit_release_ms;  /* elastic (whole-handle: whole) handles released */
+} kvpool_steps;
+
+int kvpool_last_toggle_steps(const kvpool* pool, kvpool_steps* out);
+
+/* The naive toggle the paper measures against (Section 3, "Toggle cost": a
+ * commit that creates and maps a whole handle, where the physical allocation
+ * dominates). For every layer: create one physical handle of base + elastic
+ * bytes, copy the layer's base contents into it (through a staging mapping),
+ * unmap the base handle from the layer's range, map the whole handle over
+ * [0, base + elastic), grant access, release the base handle. The layer
+ * pointers do not move and base contents are preserved bit for bit.
+ * Requires a decommitted pool (KV_ERR_STATE if it was committed with
+ * kvpool_commit_elastic; a successful no-op if committed by this call). On any
+ * failure every layer is left on its base handle and the new handles are
+ * released (KV_ERR_OOM if they could not be created). kvpool_decommit_elastic
+ * on a pool committed this way does the whole-handle decommit: new base
+ * handles, the base contents copied back, the whole handles unmapped and
+ * released. Synchronous. elapsed_ms (nullable) receives the host wall time. */
+int kvpool_commit_whole(kvpool* pool, double* elapsed_ms);
 
 /* Decommit if needed, unmap the base handles, free the ranges. NULL is a no-op. */
 void kvpool_destroy(kvpool* pool);

@@ -39,9 +39,12 @@ struct kvpool {
   std::vector<char*> va;
   std::vector<hipMemGenericAllocationHandle_t> base_h;
   std::vector<hipMemGenericAllocationHandle_t> elastic_h;
+  // Committed through one whole handle per layer over base + elastic (the
+  // naive toggle): whole_h holds those handles and base_h is empty.
+  std::vector<hipMemGenericAllocationHandle_t> whole_h;
   bool committed = false;
-  double last_create_ms = 0, last_map_ms = 0, last_access_ms = 0, last_sync_ms = 0,
-         last_unmap_ms = 0;
+  bool whole = false;
+  kvpool_steps last;   // host wall time of each step of the last commit / decommit
 };
 
 namespace {
@@ -53,6 +56,10 @@ constexpr size_t kHugePage = size_t(2) << 20;
 
 double ms_since(clock_type::time_point t0) {
   return std::chrono::duration<double, std::milli>(clock_type::now() - t0).count();
+}
+
+double ms_between(clock_type::time_point a, clock_type::time_point b) {
+  return std::chrono::duration<double, std::milli>(b - a).count();
 }
 
 hipMemAllocationProp device_prop(int device) {
@@ -105,9 +112,161 @@ void free_pool(kvpool* p) {
       if (p->base_bytes) (void)hipMemUnmap(p->va[l], p->base_bytes);
       (void)hipMemRelease(p->base_h[l]);
     }
+    if (!p->whole_h.empty() && p->whole_h[l]) {
+      (void)hipMemUnmap(p->va[l], p->base_bytes + p->elastic_bytes);
+      (void)hipMemRelease(p->whole_h[l]);
+    }
     if (p->va[l]) (void)hipMemAddressFree(p->va[l], p->reserve_bytes);
   }
   delete p;
+}
+
+// Staging ranges: one reserved range per layer, each mapped to a new handle
+// so that the layer's current contents can be copied into it before the
+// handles are swapped under the layer's own range.
+struct Staging {
+  std::vector<char*> va;
+  size_t bytes = 0;
+  std::vector<bool> mapped;
+  ~Staging() {
+    for (size_t l = 0; l < va.size(); ++l) {
+      if (mapped[l]) (void)hipMemUnmap(va[l], bytes);
+      if (va[l]) (void)hipMemAddressFree(va[l], bytes);
+    }
+  }
+};
+
+// Map handles h[l] at fresh ranges of `bytes`, copy the first `copy_bytes`
+// of each layer's range into them, and wait for the copies; the staging
+// mappings go away with st.
+int stage_and_copy(kvpool* p, const std::vector<hipMemGenericAllocationHandle_t>& h,
+                   size_t bytes, size_t copy_bytes, Staging& st) {
+  hipMemAccessDesc acc = access_desc(p->device);
+  st.bytes = bytes;
+  st.va.assign(p->num_layers, nullptr);
+  st.mapped.assign(p->num_layers, false);
+  for (int l = 0; l < p->num_layers; ++l) {
+    void* v = nullptr;
+    hipError_t e = hipMemAddressReserve(&v, bytes, p->align, nullptr, 0);
+    if (e != hipSuccess) return hip_fail(e, "hipMemAddressReserve(staging)");
+    st.va[l] = static_cast<char*>(v);
+    e = hipMemMap(st.va[l], bytes, 0, h[l], 0);
+    if (e != hipSuccess) return hip_fail(e, "hipMemMap(staging)");
+    st.mapped[l] = true;
+    e = hipMemSetAccess(st.va[l], bytes, &acc, 1);
+    if (e != hipSuccess) return hip_fail(e, "hipMemSetAccess(staging)");
+  }
+  if (copy_bytes) {
+    for (int l = 0; l < p->num_layers; ++l) {
+      hipError_t e = hipMemcpyAsync(st.va[l], p->va[l], copy_bytes, hipMemcpyDeviceToDevice,
+                                    nullptr);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(staging)");
+    }
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize(staging)");
+  }
+  return KV_OK;
+}
+
+void release_all(std::vector<hipMemGenericAllocationHandle_t>& h) {
+  for (auto& x : h) {
+    if (x) (void)hipMemRelease(x);
+    x = 0;
+  }
+}
+
+// Swap the mapping under every layer's range: [0, old_bytes) of handles
+// old_h out, [0, new_bytes) of handles new_h in. On a failure every layer is
+// put back on its old handle. Accumulates the unmap and map time.
+int swap_mappings(kvpool* p, std::vector<hipMemGenericAllocationHandle_t>& old_h,
+                  size_t old_bytes, std::vector<hipMemGenericAllocationHandle_t>& new_h,
+                  size_t new_bytes, double* unmap_ms, double* map_ms) {
+  hipMemAccessDesc acc = access_desc(p->device);
+  auto restore_old = [&](int k) {
+    if (old_bytes && hipMemMap(p->va[k], old_bytes, 0, old_h[k], 0) == hipSuccess)
+      (void)hipMemSetAccess(p->va[k], old_bytes, &acc, 1);
+  };
+  *unmap_ms = *map_ms = 0;
+  for (int l = 0; l < p->num_layers; ++l) {
+    const auto t0 = clock_type::now();
+    hipError_t e = old_bytes ? hipMemUnmap(p->va[l], old_bytes) : hipSuccess;
+    const auto t1 = clock_type::now();
+    *unmap_ms += ms_between(t0, t1);
+    const bool unmapped = e == hipSuccess;
+    if (unmapped) e = hipMemMap(p->va[l], new_bytes, 0, new_h[l], 0);
+    *map_ms += ms_between(t1, clock_type::now());
+    if (e != hipSuccess) {
+      const int rc = hip_fail(e, "swapping a layer's handles");
+      if (unmapped) restore_old(l);
+      for (int k = 0; k < l; ++k) {
+        (void)hipMemUnmap(p->va[k], new_bytes);
+        restore_old(k);
+      }
+      (void)hipGetLastError();
+      return rc;
+    }
+  }
+  return KV_OK;
+}
+
+// The whole-handle decommit (the device is synchronised): new base handles,
+// the base contents copied out of the whole handles, the handles swapped,
+// the whole handles released.
+int decommit_whole(kvpool* p) {
+  hipMemAllocationProp prop = device_prop(p->device);
+  hipMemAccessDesc acc = access_desc(p->device);
+  const size_t whole = p->base_bytes + p->elastic_bytes;
+  const auto t1 = clock_type::now();
+  std::vector<hipMemGenericAllocationHandle_t> b(p->num_layers, 0);
+  if (p->base_bytes) {
+    for (int l = 0; l < p->num_layers; ++l) {
+      hipError_t e = hipMemCreate(&b[l], p->base_bytes, &prop, 0);
+      if (e != hipSuccess) {
+        b[l] = 0;
+        release_all(b);
+        return hip_fail(e, "hipMemCreate(base)");
+      }
+    }
+  }
+  const auto t2 = clock_type::now();
+  if (p->base_bytes) {
+    Staging st;
+    const int rc = stage_and_copy(p, b, p->base_bytes, p->base_bytes, st);
+    if (rc != KV_OK) {
+      release_all(b);
+      return rc;
+    }
+  }
+  const auto t3 = clock_type::now();
+  double unmap_ms = 0, map_ms = 0;
+  int rc = KV_OK;
+  if (p->base_bytes) {
+    rc = swap_mappings(p, p->whole_h, whole, b, p->base_bytes, &unmap_ms, &map_ms);
+  } else {
+    for (int l = 0; l < p->num_layers; ++l) (void)hipMemUnmap(p->va[l], whole);
+  }
+  if (rc != KV_OK) {
+    release_all(b);
+    return rc;
+  }
+  const auto t4 = clock_type::now();
+  for (int l = 0; l < p->num_layers && p->base_bytes; ++l) {
+    hipError_t e = hipMemSetAccess(p->va[l], p->base_bytes, &acc, 1);
+    if (e != hipSuccess && rc == KV_OK) rc = hip_fail(e, "hipMemSetAccess(base)");
+  }
+  const auto t5 = clock_type::now();
+  release_all(p->whole_h);
+  const auto t6 = clock_type::now();
+  p->base_h = b;
+  p->committed = false;
+  p->whole = false;
+  p->last.decommit_create_ms = ms_between(t1, t2);
+  p->last.decommit_copy_ms = ms_between(t2, t3);
+  p->last.decommit_unmap_ms = unmap_ms;
+  p->last.decommit_map_ms = ms_between(t3, t4) - unmap_ms;
+  p->last.decommit_access_ms = ms_between(t4, t5);
+  p->last.decommit_release_ms = ms_between(t5, t6);
+  return rc;
 }
 
 }  // namespace
@@ -155,6 +314,7 @@ extern "C" int kvpool_create(int device, int num_layers, size_t base_bytes_per_l
   p->va.assign(num_layers, nullptr);
   p->base_h.assign(num_layers, 0);
   p->elastic_h.assign(num_layers, 0);
+  p->whole_h.assign(num_layers, 0);
 
   hipMemAllocationProp prop = device_prop(device);
   hipMemAccessDesc acc = access_desc(device);
@@ -258,11 +418,82 @@ extern "C" int kvpool_commit_elastic(kvpool* p, double* elapsed_ms) {
   }
   const auto t3 = clock_type::now();
   p->committed = true;
-  p->last_create_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
-  p->last_map_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
-  p->last_access_ms = std::chrono::duration<double, std::milli>(t3 - t2).count();
+  p->whole = false;
+  p->last.commit_create_ms = ms_between(t0, t1);
+  p->last.commit_copy_ms = 0;
+  p->last.commit_map_ms = ms_between(t1, t2);
+  p->last.commit_access_ms = ms_between(t2, t3);
+  p->last.commit_release_ms = 0;
   if (elapsed_ms) *elapsed_ms = ms_since(t0);
   return KV_OK;
+}
+
+extern "C" int kvpool_commit_whole(kvpool* p, double* elapsed_ms) {
+  kvattn::clear_error();
+  const auto t0 = clock_type::now();
+  if (!p) return kvattn::set_error(KV_ERR_INVALID, "kvpool_commit_whole: null pool");
+  if (p->committed) {
+    if (!p->whole)
+      return kvattn::set_error(KV_ERR_STATE,
+                               "kvpool_commit_whole: committed with two handles; decommit first");
+    if (elapsed_ms) *elapsed_ms = ms_since(t0);
+    return KV_OK;
+  }
+  if (p->elastic_bytes == 0) {
+    if (elapsed_ms) *elapsed_ms = ms_since(t0);
+    return KV_OK;
+  }
+  DeviceScope scope(p->device);
+  if (!scope.ok) return kvattn::set_error(KV_ERR_HIP, "kvpool_commit_whole: hipSetDevice failed");
+  hipMemAllocationProp prop = device_prop(p->device);
+  hipMemAccessDesc acc = access_desc(p->device);
+  const size_t whole = p->base_bytes + p->elastic_bytes;
+  // 1. physical allocation of every layer's whole range
+  std::vector<hipMemGenericAllocationHandle_t> h(p->num_layers, 0);
+  for (int l = 0; l < p->num_layers; ++l) {
+    hipError_t e = hipMemCreate(&h[l], whole, &prop, 0);
+    if (e != hipSuccess) {
+      h[l] = 0;
+      release_all(h);
+      return hip_fail(e, "hipMemCreate(whole)");
+    }
+  }
+  const auto t1 = clock_type::now();
+  // 2. the base contents copied into the new handles
+  {
+    Staging st;
+    const int rc = stage_and_copy(p, h, whole, p->base_bytes, st);
+    if (rc != KV_OK) {
+      release_all(h);
+      return rc;
+    }
+  }
+  const auto t2 = clock_type::now();
+  // 3. the layer ranges switched from the base handles to the whole handles
+  double unmap_ms = 0, map_ms = 0;
+  int rc = swap_mappings(p, p->base_h, p->base_bytes, h, whole, &unmap_ms, &map_ms);
+  if (rc != KV_OK) {
+    release_all(h);
+    return rc;
+  }
+  const auto t3 = clock_type::now();
+  for (int l = 0; l < p->num_layers; ++l) {
+    hipError_t e = hipMemSetAccess(p->va[l], whole, &acc, 1);
+    if (e != hipSuccess && rc == KV_OK) rc = hip_fail(e, "hipMemSetAccess(whole)");
+  }
+  const auto t4 = clock_type::now();
+  release_all(p->base_h);
+  const auto t5 = clock_type::now();
+  p->whole_h = h;
+  p->committed = true;
+  p->whole = true;
+  p->last.commit_create_ms = ms_between(t0, t1);
+  p->last.commit_copy_ms = ms_between(t1, t2);
+  p->last.commit_map_ms = ms_between(t2, t3);   // unmapping the base handles included
+  p->last.commit_access_ms = ms_between(t3, t4);
+  p->last.commit_release_ms = ms_between(t4, t5);
+  if (elapsed_ms) *elapsed_ms = ms_since(t0);
+  return rc;
 }
 
 extern "C" int kvpool_decommit_elastic(kvpool* p, double* elapsed_ms) {
@@ -280,17 +511,29 @@ extern "C" int kvpool_decommit_elastic(kvpool* p, double* elapsed_ms) {
   hipError_t e = hipDeviceSynchronize();
   if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
   const auto t1 = clock_type::now();
+  p->last.decommit_sync_ms = ms_between(t0, t1);
+  if (p->whole) {
+    const int rc = decommit_whole(p);
+    if (elapsed_ms) *elapsed_ms = ms_since(t0);
+    return rc;
+  }
   int rc = KV_OK;
   for (int l = 0; l < p->num_layers; ++l) {
     e = hipMemUnmap(p->va[l] + p->base_bytes, p->elastic_bytes);
     if (e != hipSuccess && rc == KV_OK) rc = hip_fail(e, "hipMemUnmap(elastic)");
+  }
+  const auto t2 = clock_type::now();
+  for (int l = 0; l < p->num_layers; ++l) {
     e = hipMemRelease(p->elastic_h[l]);
     if (e != hipSuccess && rc == KV_OK) rc = hip_fail(e, "hipMemRelease(elastic)");
     p->elastic_h[l] = 0;
   }
+  const auto t3 = clock_type::now();
   p->committed = false;
-  p->last_sync_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
-  p->last_unmap_ms = ms_since(t1);
+  p->last.decommit_create_ms = p->last.decommit_copy_ms = 0;
+  p->last.decommit_unmap_ms = ms_between(t1, t2);
+  p->last.decommit_release_ms = ms_between(t2, t3);
+  p->last.decommit_map_ms = p->last.decommit_access_ms = 0;
   if (elapsed_ms) *elapsed_ms = ms_since(t0);
   return rc;
 }
@@ -300,11 +543,18 @@ extern "C" int kvpool_last_toggle_breakdown(const kvpool* p, double* create_ms, 
                                             double* unmap_ms) {
   kvattn::clear_error();
   if (!p) return kvattn::set_error(KV_ERR_INVALID, "kvpool_last_toggle_breakdown: null pool");
-  if (create_ms) *create_ms = p->last_create_ms;
-  if (map_ms) *map_ms = p->last_map_ms;
-  if (access_ms) *access_ms = p->last_access_ms;
-  if (sync_ms) *sync_ms = p->last_sync_ms;
-  if (unmap_ms) *unmap_ms = p->last_unmap_ms;
+  if (create_ms) *create_ms = p->last.commit_create_ms;
+  if (map_ms) *map_ms = p->last.commit_map_ms;
+  if (access_ms) *access_ms = p->last.commit_access_ms;
+  if (sync_ms) *sync_ms = p->last.decommit_sync_ms;
+  if (unmap_ms) *unmap_ms = p->last.decommit_unmap_ms + p->last.decommit_release_ms;
+  return KV_OK;
+}
+
+extern "C" int kvpool_last_toggle_steps(const kvpool* p, kvpool_steps* out) {
+  kvattn::clear_error();
+  if (!p || !out) return kvattn::set_error(KV_ERR_INVALID, "kvpool_last_toggle_steps: null");
+  *out = p->last;
   return KV_OK;
 }
 

@@ -27,6 +27,16 @@ _STATUS = {0: "KV_OK", -1: "KV_ERR_INVALID", -2: "KV_ERR_UNSUPPORTED", -3: "KV_E
 
 _lib = None
 
+POOL_STEPS = ("commit_create_ms", "commit_copy_ms", "commit_map_ms", "commit_access_ms",
+              "commit_release_ms", "decommit_sync_ms", "decommit_create_ms",
+              "decommit_copy_ms", "decommit_unmap_ms", "decommit_map_ms",
+              "decommit_access_ms", "decommit_release_ms")
+
+
+class KvPoolSteps(ctypes.Structure):
+    """``kvpool_steps``: host ms of each step of a pool's last commit and decommit."""
+    _fields_ = [(n, ctypes.c_double) for n in POOL_STEPS]
+
 
 class KvAttnError(RuntimeError):
     def __init__(self, code: int, msg: str):
@@ -76,6 +86,8 @@ def lib() -> ctypes.CDLL:
        ctypes.POINTER(ctypes.c_size_t))
     _c(L.kvpool_last_toggle_breakdown, i32, vp, dp, dp, dp, dp, dp)
     _c(L.kvpool_destroy, None, vp)
+    _c(L.kvpool_commit_whole, i32, vp, dp)
+    _c(L.kvpool_last_toggle_steps, i32, vp, ctypes.POINTER(KvPoolSteps))
     _c(L.kvpool_time_single_handle, i32, i32, sz, dp, dp, dp, dp)
     ip = ctypes.POINTER(ctypes.c_int32)
     _c(L.kvblocks_create, i32, i32, i32, ctypes.POINTER(vp))
@@ -431,6 +443,20 @@ class ElasticPool:
         check(lib().kvpool_last_toggle_breakdown(self._h, *[ctypes.byref(x) for x in v]))
         return dict(zip(["create_ms", "map_ms", "access_ms", "sync_ms", "unmap_ms"],
                         [x.value for x in v]))
+
+    def commit_whole(self, empty_cache: bool = True) -> float:
+        """The naive toggle: one whole handle per layer over base + elastic,
+        base contents copied in; returns host wall ms."""
+        if empty_cache:
+            torch.cuda.empty_cache()
+        ms = ctypes.c_double()
+        check(lib().kvpool_commit_whole(self._h, ctypes.byref(ms)))
+        return ms.value
+
+    def last_steps(self) -> dict:
+        st = KvPoolSteps()
+        check(lib().kvpool_last_toggle_steps(self._h, ctypes.byref(st)))
+        return {n: getattr(st, n) for n in POOL_STEPS}
 
     @staticmethod
     def time_single_handle(nbytes: int, device: int = 0) -> dict:

@@ -10,6 +10,8 @@ free; everything is released on return.
 """
 from __future__ import annotations
 
+import time
+
 import torch
 
 from . import kvattn as K
@@ -56,8 +58,21 @@ def run(num_layers: int = 32, reserve_bytes: int = 3 << 30, margin_bytes: int = 
         except K.KvAttnError as e:
             res["recommit_without_empty_cache"] = "oom" if e.code == K.KV_ERR_OOM else str(e)
         res["pool_consistent_after_failed_commit"] = not pool.is_committed
-        res["recommit_ms"] = pool.commit(empty_cache=True)
+        # the recommit once torch has returned its cache: emptying the cache
+        # and the commit's own steps, each timed
+        torch.cuda.synchronize(device)
+        t0 = time.perf_counter()
+        torch.cuda.empty_cache()
+        res["empty_cache_ms"] = (time.perf_counter() - t0) * 1e3
+        res["recommit_ms"] = pool.commit(empty_cache=False)
+        res["recommit_steps_ms"] = {k: v for k, v in pool.last_steps().items()
+                                    if k.startswith("commit")}
         res["recommit_ok"] = pool.is_committed
+        # the same recommit once more in steady state (nothing to return)
+        pool.decommit()
+        res["steady_recommit_ms"] = pool.commit(empty_cache=False)
+        res["steady_recommit_steps_ms"] = {k: v for k, v in pool.last_steps().items()
+                                           if k.startswith("commit")}
         pool.decommit()
     finally:
         del filler

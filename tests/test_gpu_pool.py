@@ -142,3 +142,56 @@ def test_decommit_waits_for_work_in_flight():
             assert torch.equal(o.view(torch.int16), ref.view(torch.int16))
     finally:
         pool.close()
+
+
+def test_whole_handle_commit_decodes_and_keeps_base_bit_for_bit():
+    """The naive toggle: one whole handle per layer over base + elastic with
+    the base contents copied in. The layer pointer does not move, base bytes
+    survive it and its decommit, a decode over base and elastic ids matches
+    the oracle, and it refuses to run over a two-handle commit."""
+    base_blocks, el_blocks = 256, 128
+    lens = [90, 1500, 1, 640, 2048]
+    b = _elastic_batch(base_blocks, el_blocks, lens, seed=47)
+    n_base = base_blocks * BLOCK // 2                   # bf16 elements of the base part
+    pool = K.ElasticPool(2, base_blocks * BLOCK, el_blocks * BLOCK)
+    try:
+        ptrs = [pool.layer_ptr(l) for l in range(2)]
+        kv = b.kv_layer.cuda()
+        for l in range(2):
+            pool.layer_view(l, committed_part=False, dtype=torch.bfloat16).copy_(kv[:n_base])
+        torch.cuda.synchronize()
+        say("pool whole-handle commit")
+        ms = pool.commit_whole()
+        steps = pool.last_steps()
+        say("whole-handle commit ms", round(ms, 3),
+            {k: round(v, 3) for k, v in steps.items() if k.startswith("commit")})
+        assert pool.is_committed and ms > 0 and steps["commit_copy_ms"] > 0
+        assert [pool.layer_ptr(l) for l in range(2)] == ptrs
+        for l in range(2):
+            layer = pool.layer_view(l, dtype=torch.bfloat16)
+            assert torch.equal(layer[:n_base].view(torch.int16), kv[:n_base].view(torch.int16))
+            layer[n_base:].copy_(kv[n_base:])
+        d = Dev(b, kv=pool.layer_ptr(1))
+        out = d.decode()
+        torch.cuda.synchronize()
+        assert_parity(out, oracle_decode(b), "bf16", "decode over whole-handle layers",
+                      seq_bounds(b, decode=True))
+        assert pool.commit_whole() >= 0                 # no-op while committed this way
+        assert pool.commit() >= 0                       # so is the two-handle commit
+        say("pool whole-handle decommit")
+        pool.decommit()
+        steps = pool.last_steps()
+        assert not pool.is_committed and steps["decommit_copy_ms"] > 0
+        assert [pool.layer_ptr(l) for l in range(2)] == ptrs
+        for l in range(2):
+            base = pool.layer_view(l, committed_part=False, dtype=torch.bfloat16)
+            assert torch.equal(base.view(torch.int16), kv[:n_base].view(torch.int16))
+        pool.commit()                                   # the two-handle path still works
+        with pytest.raises(K.KvAttnError) as e:
+            pool.commit_whole()
+        assert e.value.code == K.KV_ERR_STATE
+        pool.decommit()
+        base = pool.layer_view(0, committed_part=False, dtype=torch.bfloat16)
+        assert torch.equal(base.view(torch.int16), kv[:n_base].view(torch.int16))
+    finally:
+        pool.close()
