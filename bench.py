@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="all",
                     choices=["all", "decode", "prefill", "mixed", "append", "two_tensor",
-                             "toggle", "elastic", "necessity", "copy"],
+                             "toggle", "controller", "elastic", "necessity", "copy"],
                     help="'all' = headline decode plus the prefill, mixed-step and toggle "
                          "legs; 'copy' = a plain 2 GiB elementwise copy, the reference that "
                          "scales the HBM byte counters")
@@ -334,44 +334,235 @@ def append_leg(args, K, work):
 
 
 def toggle_leg(K):
-    """Commit / decommit of a 3 GiB elastic reserve spread over 32 layers."""
+    """Commit / decommit of a 3 GiB elastic reserve spread over 32 layers of
+    128 MiB base each: the two-handle toggle with every step timed; when the
+    physical pages arrive (the first write to the committed elastic pages
+    against a second write); and the naive whole-handle toggle (one handle
+    per layer over base + elastic, base contents copied in and out) on the
+    same pool."""
     from workloads.configs import ELASTIC
     gran = max(K.ElasticPool.granularity(), 2 << 20)
     el = ELASTIC.elastic_bytes_per_layer
     assert el % gran == 0
     base = 64 * gran
-    pool = K.ElasticPool(ELASTIC.num_layers, base, el)
-    commit, decommit, bd_c, bd_d = [], [], [], []
+    L = ELASTIC.num_layers
+    pool = K.ElasticPool(L, base, el)
+    med = statistics.median
+    commit, decommit, st_c, st_d = [], [], [], []
+    first, second = [], []
+    whole_c, whole_d, wst_c, wst_d = [], [], [], []
     try:
+        for l in range(L):
+            pool.layer_view(l, committed_part=False).fill_(l)
+        torch.cuda.synchronize()
         for i in range(22):
             c = pool.commit()
-            bc = pool.last_breakdown()
+            sc = pool.last_steps()
             d = pool.decommit()
-            bdd = pool.last_breakdown()
+            sd = pool.last_steps()
             if i >= 2:
                 commit.append(c)
                 decommit.append(d)
-                bd_c.append(bc)
-                bd_d.append(bdd)
+                st_c.append(sc)
+                st_d.append(sd)
+        for i in range(6):
+            pool.commit()
+            views = [pool.layer_view(l)[base:] for l in range(L)]
+            times = []
+            for _ in range(2):
+                with Timer() as t:
+                    for v in views:
+                        v.fill_(1)
+                times.append(t.ms)
+            del views
+            pool.decommit()
+            if i >= 1:
+                first.append(times[0])
+                second.append(times[1])
+        for i in range(7):
+            c = pool.commit_whole()
+            sc = pool.last_steps()
+            d = pool.decommit()
+            sd = pool.last_steps()
+            if i >= 2:
+                whole_c.append(c)
+                whole_d.append(d)
+                wst_c.append(sc)
+                wst_d.append(sd)
+        base_ok = all(int(pool.layer_view(l, committed_part=False)[-1]) == l for l in range(L))
     finally:
         pool.close()
-    med = statistics.median
-    res = {"reserve_bytes": el * ELASTIC.num_layers, "layers": ELASTIC.num_layers,
-           "granularity": gran, "cycles": len(commit),
+
+    def steps(rows, prefix):
+        return {k[len(prefix):]: round(med([r[k] for r in rows]), 4) for k in rows[0]
+                if k.startswith(prefix) and med([r[k] for r in rows]) > 0}
+    res = {"reserve_bytes": el * L, "layers": L, "base_bytes_per_layer": base,
+           "elastic_bytes_per_layer": el, "granularity": gran, "cycles": len(commit),
            "commit_ms_median": med(commit), "decommit_ms_median": med(decommit),
-           "commit_breakdown_ms": {k: med([x[k] for x in bd_c])
-                                   for k in ("create_ms", "map_ms", "access_ms")},
-           "decommit_breakdown_ms": {k: med([x[k] for x in bd_d])
-                                     for k in ("sync_ms", "unmap_ms")}}
-    # the naive alternative: one handle for the whole reserve (allocation cost only:
-    # on ROCm such a handle cannot back the per-layer slices)
-    single = [K.ElasticPool.time_single_handle(el * ELASTIC.num_layers) for _ in range(5)]
+           "commit_steps_ms": steps(st_c, "commit_"),
+           "decommit_steps_ms": steps(st_d, "decommit_"),
+           "first_write_elastic_ms_median": med(first),
+           "second_write_elastic_ms_median": med(second),
+           "whole_handle": {"cycles": len(whole_c), "commit_ms_median": med(whole_c),
+                            "decommit_ms_median": med(whole_d),
+                            "commit_steps_ms": steps(wst_c, "commit_"),
+                            "decommit_steps_ms": steps(wst_d, "decommit_"),
+                            "base_contents_preserved": base_ok}}
+    # one handle of the whole reserve, created, mapped and released (the
+    # allocation cost alone; such a handle cannot back per-layer slices)
+    single = [K.ElasticPool.time_single_handle(el * L) for _ in range(5)]
     res["single_handle_reserve_ms_median"] = {
         k: med([x[k] for x in single]) for k in ("create_ms", "map_ms", "access_ms",
                                                   "release_ms")}
-    log(f"toggle: commit {res['commit_ms_median']:.2f} ms, decommit "
-        f"{res['decommit_ms_median']:.2f} ms; one {el * ELASTIC.num_layers >> 20} MiB handle: "
-        f"{res['single_handle_reserve_ms_median']}")
+    log(f"toggle: commit {res['commit_ms_median']:.2f} ms {res['commit_steps_ms']}, decommit "
+        f"{res['decommit_ms_median']:.2f} ms {res['decommit_steps_ms']}; first write "
+        f"{res['first_write_elastic_ms_median']:.2f} ms, second "
+        f"{res['second_write_elastic_ms_median']:.2f} ms; whole-handle {res['whole_handle']}")
+    return res
+
+
+def controller_leg(K, work):
+    """The toggle controller live at full reserve size: 32 layers of 1 GiB
+    base (16384 blocks) plus 96 MiB elastic (1536 blocks), 3 GiB of reserve
+    in all, hysteresis 2. A decode step over all 32 layers (48 sequences,
+    lengths U[1024, 4096], 1300 of their blocks elastic) is captured
+    in one HIP graph (kvattn_decode_noalloc, so the graph allocates nothing)
+    and replayed. Sequence: decode-only steps until the controller commits;
+    the batch takes its blocks (base first, then elastic) and is filled;
+    graph replays; a prefill is announced: the controller refuses while
+    elastic blocks are live, they are migrated to base blocks in every layer
+    (plan + block copies + table rewrite, timed as the drain), then it
+    decommits (other sequences having finished, so that base blocks are free
+    to take the migrated ones); a 3 GiB activation burst stands in for the
+    prefill; decode-only
+    steps until it recommits (torch's cache emptied first). Every replay is
+    checked bit for bit against the first."""
+    from workloads.configs import ELASTIC as E
+    L, HKV, D, HQ = E.num_layers, 8, 128, 32
+    blk = 2 * HKV * 16 * D * 2
+    nb_base, nb_el = 16384, E.elastic_blocks
+    nb = nb_base + nb_el
+    torch.cuda.empty_cache()
+    pool = K.ElasticPool(L, nb_base * blk, nb_el * blk)
+    bp = K.BlockPool(nb_base, nb_el)
+    ctl = K.Controller(pool, bp, hysteresis=2)
+    g = torch.Generator().manual_seed(2608)
+    lens = torch.randint(1024, 4097, (48,), generator=g).numpy().astype(np.int32)
+    need = int(sum((int(x) + 15) // 16 for x in lens))
+    res = {"layers": L, "base_blocks": nb_base, "elastic_blocks": nb_el,
+           "reserve_bytes": nb_el * blk * L, "num_seqs": len(lens),
+           "sum_seq_len": int(lens.sum()), "hysteresis": 2, "events": []}
+    try:
+        filler = bp.alloc(nb_base - (need - 1300))      # other sequences' base blocks
+        acts = []
+        for step in range(3):
+            a, ms = ctl.before_step(False)
+            acts.append(a)
+            if a:
+                res["events"].append({"step": step, "action": "commit", "ms": ms,
+                                      "steps_ms": pool.last_steps()})
+        assert ctl.committed, acts
+        ids = bp.alloc(need)
+        res["elastic_fraction_of_ids"] = float((ids >= nb_base).mean())
+        bt_np = np.full((len(lens), 256), -1, dtype=np.int32)
+        o = 0
+        for s_, Ls in enumerate(lens):
+            nbk = (int(Ls) + 15) // 16
+            bt_np[s_, :nbk] = ids[o:o + nbk]
+            o += nbk
+        bt = torch.from_numpy(bt_np).cuda()
+        sl = torch.from_numpy(lens).cuda()
+        idx = torch.from_numpy(ids.astype(np.int64)).cuda()
+        for l in range(L):
+            lay = pool.layer_view(l, dtype=torch.bfloat16).view(nb, blk // 2)
+            lay[idx] = torch.randn(len(ids), blk // 2, device="cuda").to(torch.bfloat16)
+        q = torch.randn(len(lens), HQ, D, generator=g).to(torch.bfloat16).cuda()
+        outs = torch.empty(L, len(lens), HQ, D, dtype=torch.bfloat16, device="cuda")
+        ptrs = [pool.layer_ptr(l) for l in range(L)]
+        scale = 1.0 / np.sqrt(D)
+
+        def step():
+            for l in range(L):
+                K.decode_noalloc(q, ptrs[l], nb, bt, sl, outs[l], num_kv_heads=HKV,
+                                 max_seq_len=4096, scale=scale)
+        step()
+        torch.cuda.synchronize()
+        ref = outs.clone()
+        graph = torch.cuda.CUDAGraph()
+        s2 = torch.cuda.Stream()
+        s2.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s2):
+            step()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=s2):
+                step()
+        torch.cuda.synchronize()
+        same = []
+
+        def replay(n):
+            ms = []
+            for _ in range(n):
+                outs.zero_()
+                torch.cuda.synchronize()
+                with Timer() as t:
+                    graph.replay()
+                ms.append(t.ms)
+                same.append(bool(torch.equal(outs.view(torch.int16), ref.view(torch.int16))))
+            return ms
+        r1 = replay(10)
+        # a prefill is announced: drain the elastic blocks by migration first
+        a, ms = None, None
+        try:
+            ctl.before_step(True)
+        except K.KvAttnError as e:
+            res["refused_while_elastic_live"] = e.code == K.KV_ERR_STATE
+        # other sequences have finished since: their base blocks are free again
+        bp.free(filler[:2000])
+        filler = filler[2000:]
+        t0 = time.perf_counter()
+        src, dst = bp.plan_drain()
+        K.copy_blocks(ptrs, nb, blk, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+        remap = np.arange(nb, dtype=np.int32)
+        remap[src] = dst
+        bt_np = np.where(bt_np >= 0, remap[np.maximum(bt_np, 0)], -1).astype(np.int32)
+        bt.copy_(torch.from_numpy(bt_np))
+        bp.free(src)
+        torch.cuda.synchronize()
+        res["drain_ms"] = (time.perf_counter() - t0) * 1e3
+        res["drained_blocks"] = int(len(src))
+        a, ms = ctl.before_step(True)
+        res["events"].append({"action": "decommit" if a == K.KVCTL_DECOMMIT else a, "ms": ms,
+                              "steps_ms": pool.last_steps()})
+        burst = torch.empty(nb_el * blk * L, dtype=torch.uint8, device="cuda")
+        burst.fill_(1)
+        torch.cuda.synchronize()
+        del burst
+        r2 = replay(10)                                  # decode over base blocks only
+        for step_i in range(3):
+            a, ms = ctl.before_step(False)
+            if a:
+                res["events"].append({"action": "commit" if a == K.KVCTL_COMMIT else a,
+                                      "ms": ms, "steps_ms": pool.last_steps()})
+        r3 = replay(10)
+        res["graph_step_ms_median"] = {"committed": statistics.median(r1),
+                                       "after_decommit": statistics.median(r2),
+                                       "after_recommit": statistics.median(r3)}
+        nbytes = work.decode_bytes(lens, HQ, HKV, D, 2) * L
+        res["graph_step_gbs"] = nbytes / (statistics.median(r1) * 1e-3) / 1e9
+        res["replays_bitwise_equal"] = all(same)
+        res["replays"] = len(same)
+        res["counts"] = dict(zip(("commits", "decommits"), ctl.counts()))
+        del filler
+    finally:
+        ctl.close()
+        bp.close()
+        pool.close()
+        torch.cuda.empty_cache()
+    for ev in res["events"]:
+        ev["steps_ms"] = {k: round(v, 4) for k, v in ev["steps_ms"].items() if v > 0}
+    log(f"controller: {res['events']}, drain {res['drain_ms']:.2f} ms "
+        f"({res['drained_blocks']} blocks), graph steps {res['graph_step_ms_median']}, "
+        f"bitwise {res['replays_bitwise_equal']}")
     return res
 
 
@@ -411,6 +602,9 @@ def elastic_leg(args, K, work):
                        device="cuda")
     reps = 3
     log(f"elastic: pool of {E.num_layers} x ({base >> 20} MiB base + {el >> 20} MiB elastic)")
+    # a hipMalloc layer allocated before the pool, so that it takes the
+    # physical memory the pool's first layers would otherwise get
+    early = torch.empty(base + el, dtype=torch.uint8, device="cuda")
     pool = K.ElasticPool(E.num_layers, base, el)
     res = {"workload": E.name, "layers": E.num_layers, "base_blocks": E.base_blocks,
            "elastic_blocks": E.elastic_blocks, "num_seqs": E.batch,
@@ -466,6 +660,29 @@ def elastic_leg(args, K, work):
         layer_ms = [per_layer_ms(bt, nb_all, [l] * 4) for l in range(E.num_layers)]
         ctl_equal = bool(torch.equal(outs[0].view(torch.int16), ref[0].view(torch.int16)))
         del ctl
+        # placement: a layer's time follows where its physical pages are,
+        # VMM or not. The hipMalloc layer allocated before the pool (early)
+        # against the pool's first layer, and one allocated now (late)
+        # against the pool's fastest layer, each alternated with its pool
+        # layer (pool, copy, copy, pool, pool, copy) over the same bytes
+        placement = {}
+        late = torch.empty(base + el, dtype=torch.uint8, device="cuda")
+        fastest = int(np.argmin(layer_ms))
+        for tag, l, cp in (("early", 0, early), ("late", fastest, late)):
+            cp.copy_(pool.layer_view(l))
+            p_runs, c_runs = [], []
+            for src in (None, cp.data_ptr(), cp.data_ptr(), None, None, cp.data_ptr()):
+                (p_runs if src is None else c_runs).append(
+                    per_layer_ms(bt, nb_all, [l] * 8, src))
+            placement[tag] = {"pool_layer": l, "pool_ms": statistics.median(p_runs),
+                              "hipmalloc_ms": statistics.median(c_runs),
+                              "pool_over_hipmalloc": statistics.median(p_runs) /
+                              statistics.median(c_runs),
+                              "runs_ms": {"pool": p_runs, "hipmalloc": c_runs}}
+        placement["slowest_pool_layer"] = {"layer": int(np.argmax(layer_ms)),
+                                           "ms": max(layer_ms)}
+        del late
+        log(f"elastic: placement control {placement}")
         # toggle cycles on the full pool, no kernels in flight
         cyc_c, cyc_d = [], []
         for _ in range(12):
@@ -473,6 +690,8 @@ def elastic_leg(args, K, work):
             cyc_c.append(pool.commit(empty_cache=False))
     finally:
         pool.close()
+        del early
+        torch.cuda.empty_cache()
     nbytes = work.decode_bytes(lens, E.num_q_heads, E.num_kv_heads, E.head_dim, 2)
     med = statistics.median
     res.update({
@@ -487,6 +706,7 @@ def elastic_leg(args, K, work):
         "layer0_x32_runs_ms": {"pool": pool_runs, "torch": ctl_runs},
         "pool_layer_ms": {"min": min(layer_ms), "median": statistics.median(layer_ms),
                           "max": max(layer_ms)},
+        "placement_control": placement,
         "roofline_committed": roofline_hbm(
             nbytes, committed, measured_traffic("traffic_decode_split_elastic_32l_b512.txt")),
         "decommitted_vs_committed_pct": 100.0 * (decommitted / committed - 1.0),
@@ -652,6 +872,8 @@ def main():
                         config={"workload": "kv_append_8192x8x128_bf16"})
     if args.workload in ("all", "toggle"):
         line["elastic_toggle"] = toggle_leg(K)
+    if args.workload in ("all", "controller"):
+        line["live_controller"] = controller_leg(K, work)
     if args.workload in ("all", "necessity"):
         line["necessity"] = necessity_leg()
     if args.workload in ("all", "elastic"):

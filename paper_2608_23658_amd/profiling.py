@@ -3,11 +3,14 @@
 ``stats``: per-kernel call count and average / total duration from a
 ``--kernel-trace --stats`` run; with ``--trace`` the per-dispatch trace of the
 same run is split by grid size, so that launches of one kernel on different
-workloads are averaged apart. ``traffic``: HBM bytes per launch of one
-kernel from two ``--pmc`` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
-dispatch), each scaled by what the same counter reads for a plain copy of a
-known number of bytes; the summary records a hash of the kernel's source so
-that a reader can tell whether the counters still describe the code.
+workloads are averaged apart. ``traffic-req``: HBM bytes per launch of one
+kernel from the L2's memory-request counts by request size (two ``--pmc``
+runs), with a plain copy of known size alongside as a check (not a scale).
+``traffic``: the older form, FETCH_SIZE / WRITE_SIZE scaled by what a plain
+copy reads. ``mfma``: MFMA utilisation and instruction mix of a bf16 matrix
+kernel from three SQ counter passes. Every summary records a hash of the
+kernel's source so that a reader can tell whether the counters still
+describe the code.
 
 The summaries are ``key = value`` text lines plus the command that produced
 the profile.
@@ -148,6 +151,140 @@ def cmd_traffic(a) -> None:
     _write(a.out, lines)
 
 
+RD = ("TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum",
+      "TCC_EA0_RDREQ_128B_sum")
+WR = ("TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum")
+
+
+def counters_per_dispatch(csv_path: str, kernel_substr: str, names,
+                          grid_size: Optional[int] = None) -> List[Dict[str, float]]:
+    """{counter: value} per dispatch of the matching kernel (values summed over
+    the rows of a dispatch)."""
+    per: Dict[str, Dict[str, float]] = {}
+    for r in _rows(csv_path):
+        name = _col(r, "Kernel_Name", "Kernel-Name", "KernelName") or ""
+        cname = _col(r, "Counter_Name", "Counter-Name", "CounterName") or ""
+        if kernel_substr not in name or cname not in names:
+            continue
+        if grid_size is not None and int(float(_col(r, "Grid_Size") or -1)) != grid_size:
+            continue
+        did = _col(r, "Dispatch_Id", "Dispatch-Id", "DispatchId") or "0"
+        d = per.setdefault(did, {})
+        d[cname] = d.get(cname, 0.0) + float(_col(r, "Counter_Value", "Counter-Value",
+                                                  "CounterValue") or 0.0)
+    return [v for v in per.values() if all(n in v for n in names)]
+
+
+def request_bytes(rd: Dict[str, float], wr: Dict[str, float]):
+    """HBM bytes from the L2's memory-request counts by size: reads are 32, 64
+    or 128 bytes each, writes 64 bytes or else 32. Returns (read bytes, write
+    bytes, read requests of no listed size)."""
+    n, n32, n64, n128 = (rd[k] for k in RD)
+    read = 32 * n32 + 64 * n64 + 128 * n128
+    w, w64 = (wr[k] for k in WR)
+    write = 64 * w64 + 32 * (w - w64)
+    return read, write, n - n32 - n64 - n128
+
+
+def cmd_traffic_req(a) -> None:
+    med = statistics.median
+    rd = counters_per_dispatch(a.rd_csv, a.kernel, RD, a.grid_size)
+    wr = counters_per_dispatch(a.wr_csv, a.kernel, WR, a.grid_size)
+    crd = counters_per_dispatch(a.copy_rd_csv, a.copy_kernel, RD)
+    cwr = counters_per_dispatch(a.copy_wr_csv, a.copy_kernel, WR)
+    if not (rd and wr and crd and cwr):
+        raise SystemExit(f"missing counter rows: {len(rd)} {len(wr)} {len(crd)} {len(cwr)}")
+    m_rd = {k: med(d[k] for d in rd) for k in RD}
+    m_wr = {k: med(d[k] for d in wr) for k in WR}
+    c_rd = {k: med(d[k] for d in crd) for k in RD}
+    c_wr = {k: med(d[k] for d in cwr) for k in WR}
+    r, w, unl = request_bytes(m_rd, m_wr)
+    cr, cw, cunl = request_bytes(c_rd, c_wr)
+    lines = [f"# HBM traffic per launch from L2 memory-request counts: {a.title}",
+             f"command_read = {a.command_rd}",
+             f"command_write = {a.command_wr}",
+             f"command_copy = {a.command_copy}",
+             f"kernel = {a.kernel}",
+             f"grid_size = {a.grid_size}",
+             f"kernel_source = {a.source}",
+             f"kernel_source_sha256 = {source_hash(a.source)}",
+             f"dispatches = {len(rd)} read, {len(wr)} write",
+             "# bytes = 32 x RDREQ_32B + 64 x RDREQ_64B + 128 x RDREQ_128B (reads);",
+             "#         64 x WRREQ_64B + 32 x (WRREQ - WRREQ_64B) (writes); no scale factor"]
+    lines += [f"{k} = {v:.0f}" for k, v in m_rd.items()]
+    lines += [f"{k} = {v:.0f}" for k, v in m_wr.items()]
+    lines += [f"read_requests_of_no_listed_size = {unl:.0f}",
+              f"check_copy_bytes = {a.copy_bytes}",
+              f"check_copy_read_bytes = {cr:.0f}",
+              f"check_copy_write_bytes = {cw:.0f}",
+              f"check_copy_read_over_known = {cr / a.copy_bytes:.4f}",
+              f"check_copy_write_over_known = {cw / a.copy_bytes:.4f}",
+              f"read_bytes_per_launch = {r:.0f}",
+              f"write_bytes_per_launch = {w:.0f}",
+              f"traffic_bytes_per_launch = {r + w:.0f}"]
+    if a.algorithmic_bytes:
+        lines.append(f"algorithmic_bytes_per_launch = {a.algorithmic_bytes}")
+        lines.append(f"traffic_over_algorithmic = {(r + w) / a.algorithmic_bytes:.4f}")
+    _write(a.out, lines)
+
+
+SQ_PASSES = {
+    "a": ("SQ_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES",
+          "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_SALU",
+          "SQ_INSTS_VALU_TRANS_F32"),
+    "b": ("SQ_INSTS_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_DATA_FIFO_FULL",
+          "SQ_LDS_CMD_FIFO_FULL", "SQ_WAIT_INST_LDS", "SQ_INSTS_SMEM", "SQ_INSTS_BRANCH"),
+    "c": ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY",
+          "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA", "SQ_INSTS_VMEM"),
+}
+
+
+def cmd_mfma(a) -> None:
+    """MFMA utilisation of a bf16 matrix kernel from three SQ counter passes."""
+    med = statistics.median
+    vals: Dict[str, float] = {}
+    for tag, path in (("a", a.pass_a), ("b", a.pass_b), ("c", a.pass_c)):
+        rows = counters_per_dispatch(path, a.kernel, SQ_PASSES[tag], a.grid_size)
+        if not rows:
+            raise SystemExit(f"no rows for pass {tag}")
+        vals.update({k: med(d[k] for d in rows) for k in SQ_PASSES[tag]})
+    mfma = vals["SQ_INSTS_MFMA"]
+    busy_cu = vals["SQ_BUSY_CU_CYCLES"]
+    simd_cycles = 4 * busy_cu                  # 4 SIMDs per CU
+    util = vals["SQ_VALU_MFMA_BUSY_CYCLES"] / simd_cycles
+    clock_ghz = busy_cu / a.num_cus / (a.kernel_us * 1e3)
+    flop_exec = vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+    lines = [f"# MFMA utilisation from SQ counters: {a.title}",
+             f"command_pass_a = {a.command_a}",
+             f"command_pass_b = {a.command_b}",
+             f"command_pass_c = {a.command_c}",
+             f"kernel = {a.kernel}",
+             f"grid_size = {a.grid_size}",
+             f"kernel_source = {a.source}",
+             f"kernel_source_sha256 = {source_hash(a.source)}",
+             "# medians per dispatch, summed over the device"]
+    lines += [f"{k} = {v:.6g}" for k, v in vals.items()]
+    lines += [
+        f"kernel_us = {a.kernel_us}",
+        f"algorithmic_flop = {a.algorithmic_flop}",
+        f"mfma_flop_executed = {flop_exec:.6g}",
+        f"mfma_flop_executed_over_algorithmic = {flop_exec / a.algorithmic_flop:.4f}",
+        f"mfma_busy_cycles_per_mfma = {vals['SQ_VALU_MFMA_BUSY_CYCLES'] / mfma:.2f}",
+        f"mfma_busy_frac_of_busy_simd_cycles = {util:.4f}",
+        f"average_shader_clock_ghz = {clock_ghz:.3f}",
+        f"tflops_frac_of_2400mhz_peak = {a.algorithmic_flop / (a.kernel_us * 1e-6) / 2516.6e12:.4f}",
+        f"busy_frac_times_clock_over_2400mhz = {util * clock_ghz / 2.4:.4f}",
+        f"valu_non_mfma_per_mfma = {(vals['SQ_INSTS_VALU'] - mfma) / mfma:.3f}",
+        f"trans_per_mfma = {vals['SQ_INSTS_VALU_TRANS_F32'] / mfma:.3f}",
+        f"salu_per_mfma = {vals['SQ_INSTS_SALU'] / mfma:.3f}",
+        f"smem_per_mfma = {vals['SQ_INSTS_SMEM'] / mfma:.3f}",
+        f"lds_per_mfma = {vals['SQ_INSTS_LDS'] / mfma:.3f}",
+        f"branch_per_mfma = {vals['SQ_INSTS_BRANCH'] / mfma:.3f}",
+        f"vmem_per_mfma = {vals['SQ_INSTS_VMEM'] / mfma:.4f}",
+    ]
+    _write(a.out, lines)
+
+
 def read_summary(path: str) -> Dict[str, str]:
     d: Dict[str, str] = {}
     with open(path) as f:
@@ -201,8 +338,36 @@ def main() -> None:
     t.add_argument("--title", required=True)
     for k in ("command_fetch", "command_write", "command_copy"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    r = sub.add_parser("traffic-req")
+    for k in ("rd_csv", "wr_csv", "copy_rd_csv", "copy_wr_csv"):
+        r.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    r.add_argument("--kernel", required=True)
+    r.add_argument("--grid-size", type=int, default=None)
+    r.add_argument("--copy-kernel", default="elementwise")
+    r.add_argument("--copy-bytes", type=int, required=True)
+    r.add_argument("--algorithmic-bytes", type=int, default=None)
+    r.add_argument("--source", required=True)
+    r.add_argument("--out", required=True)
+    r.add_argument("--title", required=True)
+    for k in ("command_rd", "command_wr", "command_copy"):
+        r.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    m = sub.add_parser("mfma")
+    for k in ("pass_a", "pass_b", "pass_c"):
+        m.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    m.add_argument("--kernel", required=True)
+    m.add_argument("--grid-size", type=int, default=None)
+    m.add_argument("--kernel-us", type=float, required=True,
+                   help="the kernel's average duration from a --kernel-trace --stats run")
+    m.add_argument("--algorithmic-flop", type=float, required=True)
+    m.add_argument("--num-cus", type=int, default=256)
+    m.add_argument("--source", required=True)
+    m.add_argument("--out", required=True)
+    m.add_argument("--title", required=True)
+    for k in ("command_a", "command_b", "command_c"):
+        m.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     a = ap.parse_args()
-    {"stats": cmd_stats, "traffic": cmd_traffic}[a.cmd](a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "traffic-req": cmd_traffic_req,
+     "mfma": cmd_mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
