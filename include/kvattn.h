@@ -174,7 +174,7 @@ const char* kvattn_trace_kernel_name(int i);
  *
  * Causal alignment is bottom-right: row i of sequence s sees keys
  * 0 .. seq_lens[s] - n_s + i. Supported: bf16, block_size 16, head_dim 128,
- * num_q_heads / num_kv_heads in {1, 2, 4}; KV_F32 returns KV_ERR_UNSUPPORTED.
+ * num_q_heads / num_kv_heads in {1, 2, 4, 8}; KV_F32 returns KV_ERR_UNSUPPORTED.
  * Asynchronous; allocates nothing.
  */
 size_t kvattn_prefill_workspace_bytes(int num_seqs, int total_q_tokens, int num_q_heads,

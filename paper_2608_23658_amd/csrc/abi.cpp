@@ -318,7 +318,7 @@ extern "C" int kvattn_prefill_chunk(const void* q, const void* kv_layer, int num
   if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
     return set_error(KV_ERR_INVALID, "kvattn_prefill_chunk: %d query heads over %d kv heads",
                      num_q_heads, num_kv_heads);
-  if (!group_ok(num_q_heads, num_kv_heads, 4))
+  if (!group_ok(num_q_heads, num_kv_heads, 8))
     return set_error(KV_ERR_UNSUPPORTED, "kvattn_prefill_chunk: group size %d not built",
                      num_q_heads / num_kv_heads);
   if (head_dim != 128)

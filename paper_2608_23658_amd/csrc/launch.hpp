@@ -75,7 +75,8 @@ hipError_t launch_prefill(const PrefillArgs& a);
 hipError_t launch_append(const AppendArgs& a);
 hipError_t launch_copy_blocks(const CopyArgs& a);
 
-// Query rows per prefill work tile (per query head).
-constexpr int kPrefillRows = 64;
+// Fewest query rows per prefill work tile (per query head): 32 at group
+// size 8; the workspace's tile list is sized for it.
+constexpr int kPrefillRows = 32;
 
 }  // namespace kvattn

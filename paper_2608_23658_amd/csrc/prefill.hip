@@ -3,7 +3,8 @@
 // chunking splits the same work; Section 1: max_num_batched_tokens bounds
 // the chunk).
 //
-// Work tile = (kv head g, 32 * 8 / G consecutive new rows of one sequence).
+// Work tile = (kv head g, 32 * 8 / G consecutive new rows of one sequence),
+// G = 1, 2, 4 or 8 query heads per kv head.
 // A workgroup of 8 wavefronts (two per SIMD) owns one tile: wave w serves
 // query head g * G + w % G over 32 rows. K/V steps of 64 keys (4 blocks) are
 // gathered through the block table straight into LDS (global_load_lds) once
@@ -716,6 +717,7 @@ hipError_t launch_prefill(const PrefillArgs& a) {
     case 1: return launch_prefill_t<1>(a);
     case 2: return launch_prefill_t<2>(a);
     case 4: return launch_prefill_t<4>(a);
+    case 8: return launch_prefill_t<8>(a);
     default: return hipErrorNotSupported;
   }
 }

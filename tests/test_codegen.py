@@ -87,8 +87,8 @@ def _functions(dis, name_part, operands=False):
 
 def test_prefill_vector_loads_are_only_the_gathers_and_q(disassembly):
     fns = _functions(disassembly, "prefill_kernel")
-    # one instance per group size (1, 2, 4) and block-offset form (shift, multiply)
-    assert len(fns) == 6, sorted(fns)
+    # one instance per group size (1, 2, 4, 8) and block-offset form (shift, multiply)
+    assert len(fns) == 8, sorted(fns)
     for name, ins in fns.items():
         vmem = [i for i in ins if re.match(r"(global|buffer|flat|scratch)_", i)]
         loads = [i for i in vmem if "load" in i]

@@ -39,17 +39,17 @@ def test_ragged_lengths_full(hq, hkv, d, dtype):
                   seq_bounds(b, decode=True))
 
 
-def test_decode_b256_full_size_sampled():
+def test_decode_b256_full_size_every_sequence():
+    """The full decode workload (256 sequences, lengths U[512, 4096]) against
+    the oracle on every sequence, gated over the whole output and per
+    sequence."""
     b = make_batch(DECODE_B256)
     say("decode 256 sequences, full size", b.num_seqs, int(b.seq_lens.sum()))
     out = Dev(b).decode()
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all()
-    rng = np.random.default_rng(0)
-    seqs = sorted(set(rng.choice(b.num_seqs, 24, replace=False).tolist()
-                      + [int(np.argmax(b.seq_lens)), int(np.argmin(b.seq_lens))]))
-    ref = oracle_decode(b, seqs=seqs)
-    assert_parity(f64(out)[seqs], ref[seqs], "bf16", "decode 256 sequences, sampled")
+    assert_parity(out, oracle_decode(b), "bf16", "decode 256 sequences, all",
+                  seq_bounds(b, decode=True))
 
 
 def test_block_permutation_bitwise():
@@ -103,20 +103,3 @@ def test_single_token_and_empty_sequences():
         want = b.v_contig[s][0].repeat_interleave(4, dim=0)
         assert torch.equal(out[s].view(torch.int16), want.view(torch.int16))
     assert (out[1] == 0).all() and (out[3] == 0).all()
-
-
-def test_out_of_range_block_ids_are_skipped():
-    """An id outside the pool contributes nothing and is never dereferenced:
-    the result equals the oracle on a table where that block's tokens are moved
-    to the end and cut off... here simply: the output stays finite and the
-    other sequences are untouched."""
-    b = make_batch_from_lens([200, 300], [1, 1], dtype="bf16", num_q_heads=8, num_kv_heads=2,
-                             head_dim=128, block_size=16, seed=12)
-    ref = oracle_decode(b)
-    d = Dev(b)
-    d.bt[0, 3] = b.num_blocks + 1000
-    say("decode bad id")
-    out = d.decode()
-    torch.cuda.synchronize()
-    assert torch.isfinite(out.float()).all()
-    assert_parity(f64(out)[1:], ref[1:], "bf16", "untouched sequence")

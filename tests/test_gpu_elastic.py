@@ -52,7 +52,7 @@ def test_elastic_decode_full_size():
     q = q_cpu.cuda()
     msl = int(lens.max())
     ws = K.workspace(K.decode_workspace_bytes(E.batch, 32, 128, msl))
-    layers = [0, 31]
+    layers = [0, 15, 31]
     say("elastic pool create", E.num_layers, base, el)
     pool = K.ElasticPool(E.num_layers, base, el)
     try:
@@ -65,8 +65,12 @@ def test_elastic_decode_full_size():
             outs[l] = K.decode(q, pool.layer_ptr(l), nb_all, bt, sl, num_kv_heads=8,
                                max_seq_len=msl, scale=E.scale, ws=ws)
         torch.cuda.synchronize()
-        # sequences with the most elastic references, plus the longest
-        seqs = sorted(set(np.argsort(-el_mask.sum(1))[:2].tolist() + [int(np.argmax(lens))]))
+        # the sequences with the most elastic references, the longest and the
+        # shortest, and ten drawn at random
+        rng = np.random.default_rng(5)
+        seqs = sorted(set(np.argsort(-el_mask.sum(1))[:4].tolist()
+                          + [int(np.argmax(lens)), int(np.argmin(lens))]
+                          + rng.choice(E.batch, 10, replace=False).tolist()))
         for l in layers:
             view = pool.layer_view(l)
             ref = np.stack([_oracle_row(view, bt_np[s], int(lens[s]), q_cpu[s]) for s in seqs])
@@ -80,6 +84,11 @@ def test_elastic_decode_full_size():
                      max_seq_len=msl, scale=E.scale, ws=ws)
         torch.cuda.synchronize()
         assert torch.isfinite(o.float()).all()
+        bt_base_np = bt_base.cpu().numpy()
+        view = pool.layer_view(0, committed_part=False)
+        dseqs = seqs[:6]
+        ref = np.stack([_oracle_row(view, bt_base_np[s], int(lens[s]), q_cpu[s]) for s in dseqs])
+        assert_parity(f64(o)[dseqs], ref, "bf16", f"elastic layer 0 decommitted, seqs {dseqs}")
         say("elastic recommit and refill")
         pool.commit()
         for l in layers:

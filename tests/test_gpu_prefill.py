@@ -20,7 +20,8 @@ def _gpu():
 
 # (24, 6) and (6, 3): kv head counts that are not powers of two, so the block
 # size is not either and block offsets take the multiply path
-@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (4, 1), (24, 6), (6, 3)])
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (4, 1), (24, 6), (6, 3),
+                                    (64, 8), (8, 1), (48, 6)])
 def test_mixed_chunks_full(hq, hkv):
     b = make_batch_from_lens(MIXED_L, MIXED_N, dtype="bf16", num_q_heads=hq, num_kv_heads=hkv,
                              head_dim=128, block_size=16, seed=31)
@@ -98,9 +99,13 @@ def test_prefill_l32768_chunk_equivalence():
                                      scale=b.scale))
     chunked = torch.cat(parts)
     torch.cuda.synchronize()
+    # one row in every 256-row tile (at a different offset in each), plus the
+    # first and last rows of the chunks and of a few tiles
     rng = np.random.default_rng(1)
-    rows = sorted(set([0, 1, 63, 64, 8191, 8192, 16383, 24576, 32767]
-                      + rng.choice(32768, 16, replace=False).tolist()))
+    rows = sorted(set([256 * t + int(o) for t, o in enumerate(rng.integers(0, 256, 128))]
+                      + [0, 1, 63, 64, 255, 256, 8191, 8192, 16383, 24576, 32767]))
+    assert len({r // 256 for r in rows}) == 128
+    say("oracle rows", len(rows))
     ref = oracle_rows(b, rows)
     assert_parity(f64(whole)[rows], ref, "bf16", "32768 whole, sampled rows")
     assert_parity(f64(chunked)[rows], ref, "bf16", "32768 as 4x8192, sampled rows")
@@ -115,9 +120,11 @@ def test_mixed_step_chunk_plus_decode():
     say("mixed step, unified call")
     uni = d.prefill(max_num_batched_tokens=8192 + 128)
     torch.cuda.synchronize()
+    # one chunk row in every 256-row tile, and every decode row
     rng = np.random.default_rng(2)
-    rows = sorted(set([0, 1, 4095, 8191] + rng.choice(8192, 8, replace=False).tolist()
-                      + (8192 + rng.choice(128, 8, replace=False)).tolist()))
+    rows = sorted(set([256 * t + int(o) for t, o in enumerate(rng.integers(0, 256, 32))]
+                      + [0, 1, 4095, 8191] + list(range(8192, 8192 + 128))))
+    say("oracle rows", len(rows))
     ref = oracle_rows(b, rows)
     assert_parity(f64(uni)[rows], ref, "bf16", "mixed step, unified")
     # decode part alone through the decode kernel

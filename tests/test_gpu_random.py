@@ -15,7 +15,7 @@ EDGES = [0, 1, 15, 16, 17, 63, 64, 65, 1023, 1024, 1025]
 DECODE_SHAPES = [(32, 8, 128, "bf16"), (8, 8, 128, "bf16"), (16, 8, 128, "bf16"),
                  (64, 8, 128, "bf16"), (8, 2, 64, "bf16"), (16, 2, 64, "bf16"),
                  (4, 2, 64, "f32"), (16, 4, 64, "f32"), (12, 3, 128, "bf16"), (24, 6, 64, "bf16")]
-PREFILL_HEADS = [(32, 8), (8, 8), (16, 8), (4, 1), (24, 6), (6, 3)]
+PREFILL_HEADS = [(32, 8), (8, 8), (16, 8), (4, 1), (24, 6), (6, 3), (64, 8), (16, 2)]
 
 
 @pytest.fixture(scope="module", autouse=True)

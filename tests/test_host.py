@@ -106,7 +106,7 @@ def test_decode_empty_batch_is_ok(L):
 @pytest.mark.parametrize("kw,code", [
     (dict(dt=K.KV_F32), K.KV_ERR_UNSUPPORTED),
     (dict(d=64), K.KV_ERR_UNSUPPORTED),
-    (dict(hq=64, hkv=8), K.KV_ERR_UNSUPPORTED),          # group of 8 is decode-only
+    (dict(hq=128, hkv=8), K.KV_ERR_UNSUPPORTED),         # group of 16 is not built
     (dict(T=200, budget=128), K.KV_ERR_INVALID),         # over max_num_batched_tokens
     (dict(cu=0), K.KV_ERR_INVALID),
     (dict(wsb=16), K.KV_ERR_INVALID),
