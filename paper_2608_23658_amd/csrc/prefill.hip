@@ -501,6 +501,10 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
     f32x16_t zero;
 #pragma unroll
     for (int e = 0; e < 16; ++e) zero[e] = 0.f;
+    // Raised issue priority while this wavefront issues its matrix slots, so
+    // that the arbiter prefers its MFMAs and operand reads over the vector
+    // work of the other wavefront of the SIMD (0.5-0.9% faster, same-box A/B).
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int k = 0; k < 32; ++k) {
       // operand reads for slot k + kAhead
@@ -533,6 +537,7 @@ void prefill_kernel(const uint16_t* __restrict__ q, const uint8_t* __restrict__ 
       if (k == 26 && do_v) gather(std::true_type{}, i + 1, idsV);
       __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_setprio(0);
     // A row without a reference yet, or a lane whose partial row sum (which
     // bounds each of its exponentials) left 2^8: take the exact row max, move
     // the reference of the rows that outgrew theirs by more than 2^8, and

@@ -249,10 +249,10 @@ def cmd_mfma(a) -> None:
             raise SystemExit(f"no rows for pass {tag}")
         vals.update({k: med(d[k] for d in rows) for k in SQ_PASSES[tag]})
     mfma = vals["SQ_INSTS_MFMA"]
-    busy_cu = vals["SQ_BUSY_CU_CYCLES"]
-    simd_cycles = 4 * busy_cu                  # 4 SIMDs per CU
-    util = vals["SQ_VALU_MFMA_BUSY_CYCLES"] / simd_cycles
-    clock_ghz = busy_cu / a.num_cus / (a.kernel_us * 1e3)
+    busy = vals["SQ_VALU_MFMA_BUSY_CYCLES"]
+    # busy fraction of the matrix pipes over the kernel's duration, counted in
+    # cycles of the 2.4 GHz clock the peak is quoted at (1024 SIMDs)
+    frac_2400 = busy / (4 * a.num_cus * a.kernel_us * 1e-6 * 2.4e9)
     flop_exec = vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
     lines = [f"# MFMA utilisation from SQ counters: {a.title}",
              f"command_pass_a = {a.command_a}",
@@ -269,11 +269,14 @@ def cmd_mfma(a) -> None:
         f"algorithmic_flop = {a.algorithmic_flop}",
         f"mfma_flop_executed = {flop_exec:.6g}",
         f"mfma_flop_executed_over_algorithmic = {flop_exec / a.algorithmic_flop:.4f}",
-        f"mfma_busy_cycles_per_mfma = {vals['SQ_VALU_MFMA_BUSY_CYCLES'] / mfma:.2f}",
-        f"mfma_busy_frac_of_busy_simd_cycles = {util:.4f}",
-        f"average_shader_clock_ghz = {clock_ghz:.3f}",
+        f"mfma_busy_cycles_per_mfma = {busy / mfma:.2f}",
+        f"mfma_busy_frac_of_2400mhz_cycles = {frac_2400:.4f}",
         f"tflops_frac_of_2400mhz_peak = {a.algorithmic_flop / (a.kernel_us * 1e-6) / 2516.6e12:.4f}",
-        f"busy_frac_times_clock_over_2400mhz = {util * clock_ghz / 2.4:.4f}",
+    ]
+    if a.clock_ghz:
+        lines += [f"shader_clock_ghz_measured = {a.clock_ghz}",
+                  f"mfma_busy_frac_of_measured_cycles = {frac_2400 * 2.4 / a.clock_ghz:.4f}"]
+    lines += [
         f"valu_non_mfma_per_mfma = {(vals['SQ_INSTS_VALU'] - mfma) / mfma:.3f}",
         f"trans_per_mfma = {vals['SQ_INSTS_VALU_TRANS_F32'] / mfma:.3f}",
         f"salu_per_mfma = {vals['SQ_INSTS_SALU'] / mfma:.3f}",
@@ -360,6 +363,8 @@ def main() -> None:
                    help="the kernel's average duration from a --kernel-trace --stats run")
     m.add_argument("--algorithmic-flop", type=float, required=True)
     m.add_argument("--num-cus", type=int, default=256)
+    m.add_argument("--clock-ghz", type=float, default=None,
+                   help="shader clock measured during the kernel, if known")
     m.add_argument("--source", required=True)
     m.add_argument("--out", required=True)
     m.add_argument("--title", required=True)
