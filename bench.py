@@ -141,6 +141,55 @@ def copy_leg(args):
             "gbs": 2 * COPY_BYTES / ms / 1e6}
 
 
+def read_ceiling(args, K, b, kv, bt, sl, nbytes, split_ms):
+    """The memory rate for decode's pattern: the read probe over the same
+    batch (the K and V tiles of every block holding a token, same grid),
+    timed over as many calls as the decode step."""
+    out = torch.empty(K.probe_read_blocks_waves(b.num_seqs, 8, b.max_seq_len) * 64,
+                      dtype=torch.int32, device="cuda")
+
+    def call():
+        K.probe_read_blocks(kv, b.num_blocks, bt, sl, num_kv_heads=8, head_dim=128,
+                            dtype=torch.bfloat16, max_seq_len=b.max_seq_len, out=out)
+
+    for _ in range(max(2, args.warmup)):
+        call()
+    with Timer() as t:
+        for _ in range(args.steps):
+            call()
+    ms = t.ms / args.steps
+    read = int(sum(-(-int(L) // 16) for L in b.seq_lens)) * 8 * 2 * 16 * 128 * 2
+    res = {"probe": "read_blocks_kernel", "ms": round(ms, 5), "bytes_read": read,
+           "read_gbs": round(read / (ms * 1e-3) / 1e9, 1),
+           "algorithmic_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "decode_split_time_over_probe": round(split_ms / ms, 4) if split_ms else None}
+    log(f"decode read probe: {ms * 1e3:.1f} us, {res['read_gbs']} GB/s of its own reads, "
+        f"decode split kernel / probe time {res['decode_split_time_over_probe']}")
+    return res
+
+
+def mfma_ceiling(args, K, prefill_tflops):
+    """The matrix-unit rate this chip sustains in the prefill kernel's launch
+    shape with random bf16 operands (the matrix probe, 8 workgroups per CU)."""
+    wg, iters = 256 * 8, 2000
+    out = torch.empty(wg * K.lib().kvattn_probe_mfma_threads(), dtype=torch.float32,
+                      device="cuda")
+    for _ in range(3):
+        K.probe_mfma(wg, iters, out=out)
+    n = max(3, args.steps // 5)
+    with Timer() as t:
+        for _ in range(n):
+            K.probe_mfma(wg, iters, out=out)
+    ms = t.ms / n
+    tf = K.probe_mfma_flops(wg, iters) / (ms * 1e-3) / 1e12
+    res = {"probe": "mfma_rate_kernel", "ms": round(ms, 4), "tflops": round(tf, 1),
+           "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+           "prefill_over_probe": round(prefill_tflops / tf, 4)}
+    log(f"matrix probe: {tf:.0f} TFLOP/s ({res['frac_of_peak']:.3f} of peak); prefill chunk "
+        f"kernel at {res['prefill_over_probe']:.3f} of it")
+    return res
+
+
 def decode_leg(args, K, work, wl):
     from workloads import DECODE_B256, make_batch
     spec = DECODE_B256
@@ -170,6 +219,7 @@ def decode_leg(args, K, work, wl):
                                  measured_traffic("traffic_decode_split_b256_l512_4096.txt")),
         "num_seqs": b.num_seqs, "sum_seq_len": int(b.seq_lens.sum()),
     }
+    res["ceiling"] = read_ceiling(args, K, b, kv, bt, sl, nbytes, kern_ms)
     return res, b
 
 
@@ -838,7 +888,7 @@ def main():
                           "block_size": 16, "parallelism": "none (1 GPU)"}
         line["roofline"] = dec["roofline"]
         line["decode"] = {k: dec[k] for k in ("kv_gbs", "bytes_per_step", "kernel_ms",
-                                              "kernel_spread_ms")}
+                                              "kernel_spread_ms", "ceiling")}
     if args.workload in ("all", "two_tensor"):
         if dec_batch is None:
             from workloads import DECODE_B256, make_batch
@@ -856,7 +906,8 @@ def main():
             "config": {"workload": "prefill_chunk8192_ctx24576_bf16", "new_tokens": 8192,
                        "cached_tokens": 24576, "num_q_heads": 32, "num_kv_heads": 8,
                        "head_dim": 128, "block_size": 16},
-            "roofline": p["roofline"], "cases": pre}
+            "roofline": p["roofline"], "cases": pre,
+            "ceiling": mfma_ceiling(args, K, p["roofline"]["achieved"])}
         if line["value"] is None:
             line.update(value=round(p["tflops"], 2), unit="TFLOP/s",
                         ms_per_step=round(p["ms_per_call"], 5), roofline=p["roofline"],

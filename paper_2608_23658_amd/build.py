@@ -22,7 +22,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["abi.cpp", "kvpool.cpp", "blockpool.cpp", "decode.hip", "prefill.hip", "append.hip",
-           "blocks.hip"]
+           "blocks.hip", "probes.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-Werror=inline-asm",
           "-I", INCLUDE, "-I", CSRC]

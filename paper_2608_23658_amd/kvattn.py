@@ -19,6 +19,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkvattn.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "kvattn.h")
+PROBES_HEADER = os.path.join(os.path.dirname(HERE), "include", "kvattn_probes.h")
 
 KV_OK, KV_ERR_INVALID, KV_ERR_UNSUPPORTED, KV_ERR_HIP, KV_ERR_OOM, KV_ERR_STATE = 0, -1, -2, -3, -4, -5
 KV_F32, KV_BF16 = 0, 1
@@ -110,15 +111,21 @@ def lib() -> ctypes.CDLL:
     _c(L.kvattn_trace_begin, i32, ctypes.POINTER(vp), i32)
     _c(L.kvattn_trace_end, i32, ctypes.POINTER(i32))
     _c(L.kvattn_trace_kernel_name, ctypes.c_char_p, i32)
+    _c(L.kvattn_probe_mfma_threads, i32)
+    _c(L.kvattn_probe_mfma, i32, vp, i32, i32, vp)
+    _c(L.kvattn_probe_read_blocks_waves, i32, i32, i32, i32)
+    _c(L.kvattn_probe_read_blocks, i32, vp, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp)
     _lib = L
     return L
 
 
 def declared_symbols() -> list:
-    """Function names declared in include/kvattn.h."""
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kv\w+)\s*\(", text)))
+    """Function names declared in include/kvattn.h and include/kvattn_probes.h."""
+    names = set()
+    for path in (HEADER, PROBES_HEADER):
+        text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
+        names.update(re.findall(r"\b(kv\w+)\s*\(", text))
+    return sorted(names)
 
 
 def last_error() -> str:
@@ -610,3 +617,54 @@ class Controller:
             self.close()
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------------------
+# Rate probes (include/kvattn_probes.h): what the chip sustains for the
+# resource each kernel is bound by, in that kernel's launch shape.
+
+def probe_mfma_flops(num_workgroups: int, iters: int) -> int:
+    """FLOP of one probe_mfma call: 8 wavefronts x 8 * iters matrix
+    instructions of 32 x 32 x 16 (32768 FLOP) per workgroup."""
+    return num_workgroups * 8 * 8 * iters * 32768
+
+
+def probe_mfma(num_workgroups: int, iters: int, out: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+    """Run the matrix-unit probe; returns each thread's accumulator sum."""
+    n = num_workgroups * int(lib().kvattn_probe_mfma_threads())
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device="cuda")
+    if out.dtype != torch.float32 or out.numel() < n:
+        raise ValueError(f"out must hold {n} float32")
+    _require_cuda(out)
+    check(lib().kvattn_probe_mfma(_ptr(out), int(num_workgroups), int(iters), _stream(stream)))
+    return out
+
+
+def probe_read_blocks_waves(num_seqs: int, num_kv_heads: int, max_seq_len: int) -> int:
+    return int(lib().kvattn_probe_read_blocks_waves(num_seqs, num_kv_heads, max_seq_len))
+
+
+def probe_read_blocks(kv_layer, num_blocks: int, block_table: torch.Tensor,
+                      seq_lens: torch.Tensor, *, num_kv_heads: int, head_dim: int,
+                      dtype: torch.dtype, max_seq_len: int,
+                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Read the K/V tiles a decode batch reads (one 32-bit word sum per lane
+    of each wavefront); returns out, int32 [waves * 64]."""
+    B = int(seq_lens.shape[0])
+    _require_int32(block_table=block_table, seq_lens=seq_lens)
+    _require_rows(B, block_table, seq_lens)
+    waves = probe_read_blocks_waves(B, num_kv_heads, max_seq_len)
+    if waves <= 0:
+        raise ValueError("invalid or too large batch for the read probe")
+    if out is None:
+        out = torch.empty(waves * 64, dtype=torch.int32, device="cuda")
+    if out.dtype != torch.int32 or out.numel() < waves * 64:
+        raise ValueError(f"out must hold {waves * 64} int32")
+    _require_cuda(kv_layer, block_table, seq_lens, out)
+    check(lib().kvattn_probe_read_blocks(_ptr(kv_layer), int(num_blocks), _ptr(block_table),
+                                         _ptr(seq_lens), B, int(num_kv_heads), int(head_dim),
+                                         _dtype_code(dtype), int(block_table.shape[1]),
+                                         int(max_seq_len), _ptr(out), _stream(stream)))
+    return out

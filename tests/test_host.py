@@ -326,3 +326,30 @@ def test_noalloc_decode_refuses_before_touching_a_device(L):
     assert call(hq=30, msl=160, mb=10) == K.KV_ERR_INVALID
     assert call(B=-1) == K.KV_ERR_INVALID
     assert call(B=0, msl=160, mb=10) == K.KV_OK          # nothing to do
+
+
+def test_probes_refuse_bad_arguments_before_any_launch(L):
+    """The rate probes check their arguments on the host; none of these
+    calls reaches a device."""
+    assert L.kvattn_probe_mfma_threads() == 512
+    assert L.kvattn_probe_mfma(None, 1, 1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_mfma(A, 0, 1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_mfma(A, 1, -1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_read_blocks_waves(256, 8, 4096) == 256 * 8 * 4
+    assert L.kvattn_probe_read_blocks_waves(256, 8, 4097) == 256 * 8 * 5
+    assert L.kvattn_probe_read_blocks_waves(0, 8, 4096) == 0
+    assert L.kvattn_probe_read_blocks_waves(1 << 20, 64, 1 << 20) == -1
+
+    def read(**kw):
+        a = dict(kv=A, nb=10, bt=A, sl=A, B=4, hkv=8, d=128, dt=K.KV_BF16, mb=10, msl=160,
+                 out=A)
+        a.update(kw)
+        return L.kvattn_probe_read_blocks(a["kv"], a["nb"], a["bt"], a["sl"], a["B"], a["hkv"],
+                                          a["d"], a["dt"], a["mb"], a["msl"], a["out"], None)
+    assert read(d=16) == K.KV_ERR_UNSUPPORTED      # a 512-byte tile
+    assert read(dt=7) == K.KV_ERR_INVALID
+    assert read(kv=A + 8) == K.KV_ERR_INVALID       # not 16-byte aligned
+    assert read(bt=None) == K.KV_ERR_INVALID
+    assert read(out=None) == K.KV_ERR_INVALID
+    assert read(B=0) == K.KV_ERR_INVALID
+    assert read(nb=0) == K.KV_ERR_INVALID
