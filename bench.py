@@ -182,11 +182,18 @@ def mfma_ceiling(args, K, prefill_tflops):
             K.probe_mfma(wg, iters, out=out)
     ms = t.ms / n
     tf = K.probe_mfma_flops(wg, iters) / (ms * 1e-3) / 1e12
+    # one more call recording each wavefront's clock: the rate with random
+    # operands is held down by the clock, not by the matrix pipes' issue
+    clocks = torch.zeros(wg * 8 * 4, dtype=torch.int64, device="cuda")
+    K.probe_mfma(wg, iters, out=out, clocks=clocks)
+    torch.cuda.synchronize()
     res = {"probe": "mfma_rate_kernel", "ms": round(ms, 4), "tflops": round(tf, 1),
            "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
            "prefill_over_probe": round(prefill_tflops / tf, 4)}
-    log(f"matrix probe: {tf:.0f} TFLOP/s ({res['frac_of_peak']:.3f} of peak); prefill chunk "
-        f"kernel at {res['prefill_over_probe']:.3f} of it")
+    res.update(K.probe_mfma_clock(clocks, iters))
+    log(f"matrix probe: {tf:.0f} TFLOP/s ({res['frac_of_peak']:.3f} of peak) at "
+        f"{res['clock_ghz_median']} GHz, matrix pipes {res['matrix_busy_median']:.3f} busy; "
+        f"prefill chunk kernel at {res['prefill_over_probe']:.3f} of it")
     return res
 
 

@@ -20,7 +20,8 @@ extern "C" {
 #endif
 
 /* Threads per workgroup of kvattn_probe_mfma (512: eight wavefronts, two per
- * SIMD, as the chunked-prefill kernel). */
+ * SIMD, as the chunked-prefill kernel; like that kernel it reserves 96 KiB of
+ * LDS, so one workgroup runs per CU). */
 int kvattn_probe_mfma_threads(void);
 
 /* Matrix-unit rate: num_workgroups workgroups, each wavefront issuing
@@ -33,12 +34,18 @@ int kvattn_probe_mfma_threads(void);
  * iteration (m = 0 .. 7) adds A[m % 4] B[(m + m / 4) % 4] to accumulator
  * m % 4.
  *
- * out   device float [num_workgroups * kvattn_probe_mfma_threads()]: each
- *       thread's sum of its 64 accumulator elements.
+ * out     device float [num_workgroups * kvattn_probe_mfma_threads()]: each
+ *         thread's sum of its 64 accumulator elements.
+ * clocks  NULL, or device uint64 [num_workgroups * 8 * 4]: wavefront w of
+ *         workgroup b writes at 4 (8 b + w) the shader clock counter
+ *         (s_memtime) before and after its loop, then the 100 MHz real-time
+ *         counter (s_memrealtime) before and after; the ratio of the two
+ *         differences, times 100 MHz, is the clock the wavefront ran at.
  * FLOP per call = num_workgroups * 8 wavefronts * 8 * iters * 32768.
  * KV_ERR_INVALID for num_workgroups <= 0, iters < 0 or a null out.
  * Asynchronous. */
-int kvattn_probe_mfma(float* out, int num_workgroups, int iters, void* stream);
+int kvattn_probe_mfma(float* out, uint64_t* clocks, int num_workgroups, int iters,
+                      void* stream);
 
 /* Wavefronts of kvattn_probe_read_blocks for a batch: one per (kv head,
  * sequence, split of 1024 context tokens), ceil(max_seq_len / 1024) splits

@@ -28,6 +28,10 @@ namespace kvattn {
 namespace {
 
 constexpr int kProbeThreads = 512;    // eight wavefronts, as the prefill kernel
+// LDS the matrix probe reserves: as the prefill kernel's, more than half of
+// the 160 KiB of a CU, so that one workgroup runs per CU and two wavefronts
+// per SIMD (its registers alone would let two workgroups share a CU)
+constexpr int kProbeLdsBytes = 96 * 1024;
 constexpr int kProbeBS = 16;          // tokens per block, as every kernel here
 constexpr int kReadSplitTokens = 1024;
 
@@ -35,7 +39,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 __global__ __attribute__((amdgpu_flat_work_group_size(kProbeThreads, kProbeThreads),
                           amdgpu_waves_per_eu(2, 2)))
-void mfma_rate_kernel(float* __restrict__ out, int iters) {
+void mfma_rate_kernel(float* __restrict__ out, unsigned long long* __restrict__ clocks,
+                      int iters) {
+  __shared__ float lds_pad[kProbeLdsBytes / 4];
   const int lane = threadIdx.x;
   // four A and four B fragments per lane from a linear congruential sequence
   // seeded by the thread's global index, values in [-1, 1)
@@ -55,6 +61,10 @@ void mfma_rate_kernel(float* __restrict__ out, int iters) {
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[j][i] = 0.f;
+  // the shader clock counter and the 100 MHz real-time counter around the
+  // loop: their ratio is the clock the chip ran the wavefront at
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
   // per iteration 8 instructions, two per accumulator, each pairing A
   // fragment m % 4 with B fragment (m + m / 4) % 4
   for (int it = 0; it < iters; ++it) {
@@ -63,12 +73,24 @@ void mfma_rate_kernel(float* __restrict__ out, int iters) {
       acc[m % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m % 4], b[(m + m / 4) % 4],
                                                            acc[m % 4], 0, 0, 0);
   }
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int i = 0; i < 16; ++i) s += acc[j][i];
-  out[(size_t)blockIdx.x * kProbeThreads + lane] = s;
+  // the sum passes through the reserved LDS, which keeps it allocated
+  lds_pad[lane] = s;
+  __syncthreads();
+  out[(size_t)blockIdx.x * kProbeThreads + lane] = lds_pad[lane];
+  if (clocks != nullptr && lane % kWave == 0) {
+    unsigned long long* c = clocks + ((size_t)blockIdx.x * (kProbeThreads / kWave) + lane / kWave) * 4;
+    c[0] = t0;
+    c[1] = t1;
+    c[2] = r0;
+    c[3] = r1;
+  }
 }
 
 __global__ __launch_bounds__(64) void read_blocks_kernel(
@@ -120,14 +142,16 @@ using kvattn::set_error;
 
 extern "C" int kvattn_probe_mfma_threads(void) { return kvattn::kProbeThreads; }
 
-extern "C" int kvattn_probe_mfma(float* out, int num_workgroups, int iters, void* stream) {
+extern "C" int kvattn_probe_mfma(float* out, uint64_t* clocks, int num_workgroups, int iters,
+                                 void* stream) {
   clear_error();
   if (num_workgroups <= 0 || iters < 0)
     return set_error(KV_ERR_INVALID, "kvattn_probe_mfma: %d workgroups, %d iterations",
                      num_workgroups, iters);
   if (!out) return set_error(KV_ERR_INVALID, "kvattn_probe_mfma: null output");
   hipLaunchKernelGGL(kvattn::mfma_rate_kernel, dim3(num_workgroups), dim3(kvattn::kProbeThreads),
-                     0, static_cast<hipStream_t>(stream), out, iters);
+                     0, static_cast<hipStream_t>(stream), out,
+                     reinterpret_cast<unsigned long long*>(clocks), iters);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? KV_OK : kvattn::hip_fail(e, "kvattn_probe_mfma launch");
 }

@@ -112,7 +112,7 @@ def lib() -> ctypes.CDLL:
     _c(L.kvattn_trace_end, i32, ctypes.POINTER(i32))
     _c(L.kvattn_trace_kernel_name, ctypes.c_char_p, i32)
     _c(L.kvattn_probe_mfma_threads, i32)
-    _c(L.kvattn_probe_mfma, i32, vp, i32, i32, vp)
+    _c(L.kvattn_probe_mfma, i32, vp, vp, i32, i32, vp)
     _c(L.kvattn_probe_read_blocks_waves, i32, i32, i32, i32)
     _c(L.kvattn_probe_read_blocks, i32, vp, i32, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp)
     _lib = L
@@ -630,16 +630,34 @@ def probe_mfma_flops(num_workgroups: int, iters: int) -> int:
 
 
 def probe_mfma(num_workgroups: int, iters: int, out: Optional[torch.Tensor] = None,
-               stream=None) -> torch.Tensor:
-    """Run the matrix-unit probe; returns each thread's accumulator sum."""
+               clocks: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Run the matrix-unit probe; returns each thread's accumulator sum. With
+    ``clocks`` (int64 [num_workgroups * 8 * 4]) each wavefront also records
+    its shader-clock and real-time counters around its loop."""
     n = num_workgroups * int(lib().kvattn_probe_mfma_threads())
     if out is None:
         out = torch.empty(n, dtype=torch.float32, device="cuda")
     if out.dtype != torch.float32 or out.numel() < n:
         raise ValueError(f"out must hold {n} float32")
-    _require_cuda(out)
-    check(lib().kvattn_probe_mfma(_ptr(out), int(num_workgroups), int(iters), _stream(stream)))
+    if clocks is not None and (clocks.dtype != torch.int64 or
+                               clocks.numel() < num_workgroups * 8 * 4):
+        raise ValueError(f"clocks must hold {num_workgroups * 8 * 4} int64")
+    _require_cuda(out, clocks)
+    check(lib().kvattn_probe_mfma(_ptr(out), _ptr(clocks), int(num_workgroups), int(iters),
+                                  _stream(stream)))
     return out
+
+
+def probe_mfma_clock(clocks: torch.Tensor, iters: int) -> dict:
+    """Median clock (GHz) of the probe's wavefronts and the matrix pipes'
+    busy fraction at that clock (two wavefronts per SIMD, 32 cycles per
+    instruction), from the counters ``probe_mfma`` recorded."""
+    c = clocks.view(-1, 4).cpu().double()
+    dt, dr = c[:, 1] - c[:, 0], c[:, 3] - c[:, 2]
+    ok = dr > 0
+    ghz = (dt[ok] / dr[ok] * 0.1).median().item()
+    busy = (2 * 8 * iters * 32 / dt[ok]).median().item()
+    return {"clock_ghz_median": round(ghz, 3), "matrix_busy_median": round(busy, 4)}
 
 
 def probe_read_blocks_waves(num_seqs: int, num_kv_heads: int, max_seq_len: int) -> int:

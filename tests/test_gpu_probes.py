@@ -77,8 +77,14 @@ def test_matrix_probe_multiplies_its_operands():
     wg, iters = 3, 5
     threads = K.lib().kvattn_probe_mfma_threads()
     say("matrix probe", wg, iters)
-    out = K.probe_mfma(wg, iters)
+    clocks = torch.zeros(wg * 8 * 4, dtype=torch.int64, device="cuda")
+    out = K.probe_mfma(wg, iters, clocks=clocks)
     torch.cuda.synchronize()
+    # every wavefront recorded increasing counters, and a clock in a sane range
+    c = clocks.view(-1, 4).cpu()
+    assert bool((c[:, 1] > c[:, 0]).all()) and bool((c[:, 3] >= c[:, 2]).all())
+    ck = K.probe_mfma_clock(clocks, iters)
+    assert 0.3 < ck["clock_ghz_median"] < 3.0, ck
     got = out.double().cpu().numpy().reshape(wg, threads // 64, 64)
     for w in range(wg):
         for v in range(threads // 64):

@@ -332,9 +332,9 @@ def test_probes_refuse_bad_arguments_before_any_launch(L):
     """The rate probes check their arguments on the host; none of these
     calls reaches a device."""
     assert L.kvattn_probe_mfma_threads() == 512
-    assert L.kvattn_probe_mfma(None, 1, 1, None) == K.KV_ERR_INVALID
-    assert L.kvattn_probe_mfma(A, 0, 1, None) == K.KV_ERR_INVALID
-    assert L.kvattn_probe_mfma(A, 1, -1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_mfma(None, None, 1, 1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_mfma(A, None, 0, 1, None) == K.KV_ERR_INVALID
+    assert L.kvattn_probe_mfma(A, A, 1, -1, None) == K.KV_ERR_INVALID
     assert L.kvattn_probe_read_blocks_waves(256, 8, 4096) == 256 * 8 * 4
     assert L.kvattn_probe_read_blocks_waves(256, 8, 4097) == 256 * 8 * 5
     assert L.kvattn_probe_read_blocks_waves(0, 8, 4096) == 0
