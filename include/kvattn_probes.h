@@ -57,15 +57,16 @@ int kvattn_probe_read_blocks_waves(int num_seqs, int num_kv_heads, int max_seq_l
  * of sequence s (blocks 0 .. ceil(L_s / 16) - 1; ids outside
  * [0, num_blocks) are skipped), laid out as kvattn_decode reads them (same
  * layer layout, block_size 16, same grid order: kv head fastest, split
- * slowest), with 16-byte non-temporal loads of 1 KiB per instruction: lane l
+ * slowest, steps of 64 tokens whose loads are all issued before any is
+ * used), with 16-byte non-temporal loads of 1 KiB per instruction: lane l
  * of a wavefront reads bytes [1024 c + 16 l, 1024 c + 16 l + 16) of each
- * tile, c = 0 .. tile_bytes / 1024 - 1.
+ * tile, c = 0 .. 3.
  *
  * kv_layer, num_blocks, block_table, seq_lens, num_seqs, num_kv_heads,
  * head_dim, max_blocks_per_seq, max_seq_len: as for kvattn_decode (L_s is
  * seq_lens[s] clamped to [0, min(max_seq_len, 16 * max_blocks_per_seq)]);
- * the tile, 16 * head_dim elements of dtype, must be a multiple of 1 KiB
- * (KV_ERR_UNSUPPORTED otherwise).
+ * the tile, 16 * head_dim elements of dtype, must be 4 KiB (bf16 with
+ * head_dim 128, fp32 with head_dim 64; KV_ERR_UNSUPPORTED otherwise).
  * out   device uint32 [kvattn_probe_read_blocks_waves(...) * 64]: lane l of
  *       wavefront w writes out[64 w + l], the sum modulo 2^32 of the 32-bit
  *       words it read (0 for a wavefront whose split holds no token).

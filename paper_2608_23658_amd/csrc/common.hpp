@@ -67,6 +67,17 @@ __device__ __forceinline__ float wave_max(float x) {
   const auto r32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
   return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
+// Sum over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the same lane of each row of
+// 16), in every lane: the gfx950 row swaps (rows 0<->1 and 2<->3, then the
+// two halves of the wavefront). The four lanes get bit-identical results.
+__device__ __forceinline__ float cross_row_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const uint32_t v = __float_as_uint(x);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
 __device__ __forceinline__ float wave_sum(float x) {
   x += dpp_mov<kDppQuadSwap1>(x);
   x += dpp_mov<kDppQuadSwap2>(x);

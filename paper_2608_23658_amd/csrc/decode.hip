@@ -10,18 +10,25 @@
 // late splits only long sequences have. The G query heads sharing the kv
 // head are served by every K/V byte read (grouped-query sharing). The
 // wavefront walks its split in steps of 64 tokens (4 blocks of 16):
-//   * K: lane t owns token t of the step. With the chunk-major K tile, the 16
-//     lanes of one block read 256 contiguous bytes per 16-byte load, and each
-//     lane ends up holding its token's whole row, so q.k needs no cross-lane
-//     reduction. q sits in LDS and every lane reads the same 16 bytes at a
-//     time (a broadcast).
+//   * loads: each block's K tile and V tile are read as they lie in memory,
+//     1 KiB per 16-byte load (K and V are read once, so the loads are
+//     non-temporal), and the K and V loads of a block are issued together.
+//     Reading K lane-per-token instead (four 256-byte pieces from four blocks
+//     per load), or all K loads before all V loads, measured 4-6% slower:
+//     the memory system serves a block's two tiles best when they are asked
+//     for at once.
+//   * K: with the chunk-major K tile, load i of a block gives lane l chunk
+//     4 i + l / 16 of token slot l % 16, a quarter of that token's row. Each
+//     lane dots its quarters of the rows of the four tokens in its slot (one
+//     per block) with the same dims of q (read from LDS), and the four lanes
+//     of a slot add their quarters with two row swaps. Lane t then takes the
+//     score of token t of the step (block t / 16, slot t % 16).
 //   * softmax: wavefront max per head (DPP and lane-row swaps), exp2 in the
 //     log2 domain, lane-local partial sums, one rescale of the accumulators
 //     per step.
-//   * V: with the dim-major V tile each 16-byte load is a 1 KiB contiguous
-//     stretch (K and V are read once, so their loads are non-temporal); lane l owns dim rows l / R (R = 16-byte chunks per row) and a
-//     run of consecutive tokens, so for bf16 p.v is a bf16 dot2 over token
-//     pairs. p reaches those lanes through LDS.
+//   * V: in the dim-major V tile lane l owns dim rows l / R (R = 16-byte
+//     chunks per row) and a run of consecutive tokens, so for bf16 p.v is a
+//     bf16 dot2 over token pairs. p reaches those lanes through LDS.
 // Only the last step of a split can hold slots past the sequence's length,
 // whose contents are arbitrary (possibly NaN); that step masks them. Partials
 // (m, l, o) of every split go to the workspace; a second kernel merges them
@@ -115,7 +122,6 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
   }
 
   const int kj = lane / S::kBS;   // block of this lane's token within the step
-  const int kr = lane % S::kBS;   // its slot
   const int vrc = lane % S::kR;   // this lane's chunk of a V dim row
 
   // Steps of 64 tokens; in the last one (kTail) the step may end inside a
@@ -138,55 +144,73 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     for (int j = 1; j < S::kTB; ++j) my_b = (kj == j) ? bid[j] : my_b;
     const bool kvalid = (!kTail || tb + lane < t1) && (my_b >= 0);
 
-    // ---- loads: K rows (lane per token), V dim rows ----
-    uint4 kreg[S::kKCh];
-    if (kvalid) {
-      const uint4* kp = reinterpret_cast<const uint4*>(block_ptr(my_b) + head_off) + kr;
-#pragma unroll
-      for (int c = 0; c < S::kKCh; ++c) kreg[c] = load_nt(kp + c * S::kBS);
-    } else {
-#pragma unroll
-      for (int c = 0; c < S::kKCh; ++c) kreg[c] = make_uint4(0, 0, 0, 0);
-    }
+    // ---- loads: each block's K tile and V tile as they lie in memory, 1 KiB
+    // per load, the two tiles of a block issued together ----
+    // K piece i of a block gives lane l the 16-byte chunk 4 i + l / 16 of the
+    // block's token slot l % 16: a quarter of that token's row.
+    uint4 kreg[S::kTB][S::kVI];
     uint4 vreg[S::kTB][S::kVI];
 #pragma unroll
     for (int j = 0; j < S::kTB; ++j) {
       if (bid[j] >= 0) {
-        const uint4* vp = reinterpret_cast<const uint4*>(block_ptr(bid[j]) + v_off) + lane;
+        const uint8_t* bp = block_ptr(bid[j]);
+        const uint4* kp = reinterpret_cast<const uint4*>(bp + head_off) + lane;
+        const uint4* vp = reinterpret_cast<const uint4*>(bp + v_off) + lane;
 #pragma unroll
-        for (int i = 0; i < S::kVI; ++i) vreg[j][i] = load_nt(vp + i * kWave);
+        for (int i = 0; i < S::kVI; ++i) {
+          kreg[j][i] = load_nt(kp + i * kWave);
+          vreg[j][i] = load_nt(vp + i * kWave);
+        }
       } else {
 #pragma unroll
-        for (int i = 0; i < S::kVI; ++i) vreg[j][i] = make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < S::kVI; ++i) {
+          kreg[j][i] = make_uint4(0, 0, 0, 0);
+          vreg[j][i] = make_uint4(0, 0, 0, 0);
+        }
       }
     }
 
-    // ---- scores: q . k for the G heads, lane-local ----
-    float sc[G];
+    // ---- scores: each lane dots its quarter of the rows of the four tokens
+    // in its slot (one per block) with the same dims of q, then the four
+    // lanes of a slot (l, l ^ 16, l ^ 32, l ^ 48) add their quarters ----
+    float part[S::kTB][G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) sc[h] = 0.f;
+    for (int j = 0; j < S::kTB; ++j)
 #pragma unroll
-    for (int c = 0; c < S::kKCh; ++c) {
-      const uint4 k = kreg[c];
+      for (int h = 0; h < G; ++h) part[j][h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < S::kVI; ++i) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const uint4 qc = q_lds[h * S::kKCh + c];
-        if constexpr (BF16) {
-          float a = sc[h];
-          a = dot2_bf16(k.x, qc.x, a);
-          a = dot2_bf16(k.y, qc.y, a);
-          a = dot2_bf16(k.z, qc.z, a);
-          a = dot2_bf16(k.w, qc.w, a);
-          sc[h] = a;
-        } else {
-          float a = sc[h];
-          a = fmaf(__uint_as_float(k.x), __uint_as_float(qc.x), a);
-          a = fmaf(__uint_as_float(k.y), __uint_as_float(qc.y), a);
-          a = fmaf(__uint_as_float(k.z), __uint_as_float(qc.z), a);
-          a = fmaf(__uint_as_float(k.w), __uint_as_float(qc.w), a);
-          sc[h] = a;
+        const uint4 qc = q_lds[h * S::kKCh + 4 * i + kj];
+#pragma unroll
+        for (int j = 0; j < S::kTB; ++j) {
+          const uint4 k = kreg[j][i];
+          float a = part[j][h];
+          if constexpr (BF16) {
+            a = dot2_bf16(k.x, qc.x, a);
+            a = dot2_bf16(k.y, qc.y, a);
+            a = dot2_bf16(k.z, qc.z, a);
+            a = dot2_bf16(k.w, qc.w, a);
+          } else {
+            a = fmaf(__uint_as_float(k.x), __uint_as_float(qc.x), a);
+            a = fmaf(__uint_as_float(k.y), __uint_as_float(qc.y), a);
+            a = fmaf(__uint_as_float(k.z), __uint_as_float(qc.z), a);
+            a = fmaf(__uint_as_float(k.w), __uint_as_float(qc.w), a);
+          }
+          part[j][h] = a;
         }
       }
+    }
+    // this lane's token is slot lane % 16 of block kj
+    float sc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+#pragma unroll
+      for (int j = 0; j < S::kTB; ++j) part[j][h] = cross_row_sum(part[j][h]);
+      sc[h] = part[0][h];
+#pragma unroll
+      for (int j = 1; j < S::kTB; ++j) sc[h] = (kj == j) ? part[j][h] : sc[h];
     }
 
     // ---- online softmax over the step (log2 domain) ----

@@ -347,6 +347,7 @@ def test_probes_refuse_bad_arguments_before_any_launch(L):
         return L.kvattn_probe_read_blocks(a["kv"], a["nb"], a["bt"], a["sl"], a["B"], a["hkv"],
                                           a["d"], a["dt"], a["mb"], a["msl"], a["out"], None)
     assert read(d=16) == K.KV_ERR_UNSUPPORTED      # a 512-byte tile
+    assert read(d=64) == K.KV_ERR_UNSUPPORTED      # bf16 with head_dim 64: 2 KiB tiles
     assert read(dt=7) == K.KV_ERR_INVALID
     assert read(kv=A + 8) == K.KV_ERR_INVALID       # not 16-byte aligned
     assert read(bt=None) == K.KV_ERR_INVALID
