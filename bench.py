@@ -658,6 +658,44 @@ def elastic_leg(args, K, work):
     outs = torch.empty(E.num_layers, E.batch, E.num_q_heads, E.head_dim, dtype=bf16,
                        device="cuda")
     reps = 3
+
+    def calls_ms(src, table, n=8):
+        for _ in range(2):
+            K.decode(q, src, nb_all, table, sl, num_kv_heads=E.num_kv_heads, max_seq_len=msl,
+                     scale=E.scale, out=outs[0], ws=ws)
+        with Timer() as t:
+            for _ in range(n):
+                K.decode(q, src, nb_all, table, sl, num_kv_heads=E.num_kv_heads,
+                         max_seq_len=msl, scale=E.scale, out=outs[0], ws=ws)
+        return t.ms / n
+
+    # The mapping itself, like for like, before anything else of this leg is
+    # allocated: a one-layer pool (base and elastic handle over one range) and
+    # a hipMalloc copy of its bytes, read through the committed table (the hot
+    # elastic set in the elastic handle) and the decommitted one (the same set
+    # on base ids), alternated (pool, copy, copy, pool, pool, copy).
+    mapping = {}
+    one = K.ElasticPool(1, base, el)
+    try:
+        one.commit()
+        fill_layer(one.layer_view(0, dtype=bf16), 0, base // 2)
+        cp1 = torch.empty(base + el, dtype=torch.uint8, device="cuda")
+        cp1.copy_(one.layer_view(0))
+        p0 = one.layer_ptr(0)
+        for tname, table in (("committed_table", bt), ("decommitted_table", bt_base)):
+            p_runs, c_runs = [], []
+            for src in (p0, cp1.data_ptr(), cp1.data_ptr(), p0, p0, cp1.data_ptr()):
+                (p_runs if src == p0 else c_runs).append(calls_ms(src, table))
+            mapping[tname] = {"pool_ms": statistics.median(p_runs),
+                              "hipmalloc_ms": statistics.median(c_runs),
+                              "pool_over_hipmalloc": statistics.median(p_runs) /
+                              statistics.median(c_runs),
+                              "runs_ms": {"pool": p_runs, "hipmalloc": c_runs}}
+        del cp1
+    finally:
+        one.close()
+    torch.cuda.empty_cache()
+    log(f"elastic: one-layer mapping control {mapping}")
     log(f"elastic: pool of {E.num_layers} x ({base >> 20} MiB base + {el >> 20} MiB elastic)")
     # a hipMalloc layer allocated before the pool, so that it takes the
     # physical memory the pool's first layers would otherwise get
@@ -763,6 +801,7 @@ def elastic_leg(args, K, work):
         "layer0_x32_runs_ms": {"pool": pool_runs, "torch": ctl_runs},
         "pool_layer_ms": {"min": min(layer_ms), "median": statistics.median(layer_ms),
                           "max": max(layer_ms)},
+        "mapping_control_one_layer": mapping,
         "placement_control": placement,
         "roofline_committed": roofline_hbm(
             nbytes, committed, measured_traffic("traffic_decode_split_elastic_32l_b512.txt")),
