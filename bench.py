@@ -672,29 +672,34 @@ def elastic_leg(args, K, work):
     # The mapping itself, like for like, before anything else of this leg is
     # allocated: a one-layer pool (base and elastic handle over one range) and
     # a hipMalloc copy of its bytes, read through the committed table (the hot
-    # elastic set in the elastic handle) and the decommitted one (the same set
-    # on base ids), alternated (pool, copy, copy, pool, pool, copy).
-    mapping = {}
-    one = K.ElasticPool(1, base, el)
-    try:
-        one.commit()
-        fill_layer(one.layer_view(0, dtype=bf16), 0, base // 2)
+    # elastic set in the elastic handle), alternated (pool, copy, copy, pool).
+    # Where an allocation's physical pages land moves its time by a few
+    # percent either way, so the pair is allocated afresh six times, in
+    # alternating order, and the ratio is reported over the six pairs.
+    ratios, pairs = [], []
+    for trial in range(6):
+        one = K.ElasticPool(1, base, el) if trial % 2 == 0 else None
         cp1 = torch.empty(base + el, dtype=torch.uint8, device="cuda")
-        cp1.copy_(one.layer_view(0))
-        p0 = one.layer_ptr(0)
-        for tname, table in (("committed_table", bt), ("decommitted_table", bt_base)):
+        if one is None:
+            one = K.ElasticPool(1, base, el)
+        try:
+            one.commit(empty_cache=False)
+            fill_layer(one.layer_view(0, dtype=bf16), 0, base // 2)
+            cp1.copy_(one.layer_view(0))
+            p0 = one.layer_ptr(0)
             p_runs, c_runs = [], []
-            for src in (p0, cp1.data_ptr(), cp1.data_ptr(), p0, p0, cp1.data_ptr()):
-                (p_runs if src == p0 else c_runs).append(calls_ms(src, table))
-            mapping[tname] = {"pool_ms": statistics.median(p_runs),
-                              "hipmalloc_ms": statistics.median(c_runs),
-                              "pool_over_hipmalloc": statistics.median(p_runs) /
-                              statistics.median(c_runs),
-                              "runs_ms": {"pool": p_runs, "hipmalloc": c_runs}}
-        del cp1
-    finally:
-        one.close()
-    torch.cuda.empty_cache()
+            for src in (p0, cp1.data_ptr(), cp1.data_ptr(), p0):
+                (p_runs if src == p0 else c_runs).append(calls_ms(src, bt))
+            pm, cm = statistics.mean(p_runs), statistics.mean(c_runs)
+            ratios.append(pm / cm)
+            pairs.append({"pool_first": trial % 2 == 0, "pool_ms": pm, "hipmalloc_ms": cm})
+        finally:
+            one.close()
+            del cp1
+            torch.cuda.empty_cache()
+    mapping = {"pool_over_hipmalloc_median": statistics.median(ratios),
+               "pool_over_hipmalloc_min": min(ratios), "pool_over_hipmalloc_max": max(ratios),
+               "pairs": pairs}
     log(f"elastic: one-layer mapping control {mapping}")
     log(f"elastic: pool of {E.num_layers} x ({base >> 20} MiB base + {el >> 20} MiB elastic)")
     # a hipMalloc layer allocated before the pool, so that it takes the
