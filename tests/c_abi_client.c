@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include "kvattn.h"
+#include "kvattn_probes.h"
 
 static int failed = 0;
 
@@ -17,6 +18,9 @@ static void check(int ok, const char* what) {
 
 int main(void) {
   check(kvattn_abi_version() == 1, "abi version");
+  check(kvattn_probe_mfma_threads() == 512, "matrix probe workgroup size");
+  check(kvattn_probe_read_blocks_waves(256, 8, 4096) == 8192, "read probe grid");
+  check(kvattn_probe_mfma(NULL, NULL, 1, 1, NULL) == KV_ERR_INVALID, "matrix probe refuses a null output");
 
   /* workspace: at least the (m, l, o) partials of every split */
   {
