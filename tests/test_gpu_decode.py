@@ -26,7 +26,8 @@ def test_tiny_decode_f32_full():
 
 @pytest.mark.parametrize("hq,hkv,d,dtype", [
     (32, 8, 128, "bf16"), (8, 8, 128, "bf16"), (16, 8, 128, "bf16"), (64, 8, 128, "bf16"),
-    (8, 2, 64, "bf16"), (4, 4, 64, "bf16"), (16, 2, 64, "bf16"), (12, 3, 128, "bf16"),
+    (8, 2, 64, "bf16"), (4, 4, 64, "bf16"), (8, 4, 64, "bf16"), (16, 2, 64, "bf16"),
+    (12, 3, 128, "bf16"),
     (4, 2, 64, "f32"), (8, 8, 64, "f32"), (16, 4, 64, "f32"), (16, 2, 64, "f32"),
 ])
 def test_ragged_lengths_full(hq, hkv, d, dtype):
