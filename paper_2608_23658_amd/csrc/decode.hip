@@ -54,6 +54,7 @@ struct DecodeShape {
   static constexpr int kTileElems = kBS * D;      // one (block, K/V, head) tile
   static constexpr int kPWords = BF16 ? (kTile / 2) * G : kTile * G;
   static_assert(kVI * 1024 == kTileElems * kEsz, "V tile is kVI loads of 1 KiB");
+  static_assert(kKCh == 4 * kVI, "a K load of 1 KiB holds a quarter of each of 16 rows");
 };
 
 // kTwo: the layer is split over two tensors (the design the paper rejects in
