@@ -122,7 +122,9 @@ __global__ __launch_bounds__(64) void decode_split_kernel(
     for (int i = 0; i < S::kVI; ++i) acc[i][h] = 0.f;
   }
 
-  const int kj = lane / S::kBS;   // block of this lane's token within the step
+  // block of this lane's token within the step, and which quarter of the K
+  // rows of its slot the lane holds
+  const int kj = lane / S::kBS;
   const int vrc = lane % S::kR;   // this lane's chunk of a V dim row
 
   // Steps of 64 tokens; in the last one (kTail) the step may end inside a
