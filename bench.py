@@ -190,9 +190,9 @@ def mfma_ceiling(args, K, prefill_tflops):
     res = {"probe": "mfma_rate_kernel", "ms": round(ms, 4), "tflops": round(tf, 1),
            "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
            "prefill_over_probe": round(prefill_tflops / tf, 4)}
-    res.update(K.probe_mfma_clock(clocks, iters))
-    log(f"matrix probe: {tf:.0f} TFLOP/s ({res['frac_of_peak']:.3f} of peak) at "
-        f"{res['clock_ghz_median']} GHz, matrix pipes {res['matrix_busy_median']:.3f} busy; "
+    res.update(K.probe_mfma_clock(clocks, iters, tf))
+    log(f"matrix probe: {tf:.0f} TFLOP/s ({res['frac_of_peak']:.3f} of peak), matrix pipes "
+        f"{res['matrix_busy_median']:.3f} busy, so a clock of {res['clock_ghz_implied']} GHz; "
         f"prefill chunk kernel at {res['prefill_over_probe']:.3f} of it")
     return res
 

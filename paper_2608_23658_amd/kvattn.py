@@ -648,16 +648,24 @@ def probe_mfma(num_workgroups: int, iters: int, out: Optional[torch.Tensor] = No
     return out
 
 
-def probe_mfma_clock(clocks: torch.Tensor, iters: int) -> dict:
-    """Median clock (GHz) of the probe's wavefronts and the matrix pipes'
-    busy fraction at that clock (two wavefronts per SIMD, 32 cycles per
-    instruction), from the counters ``probe_mfma`` recorded."""
+def probe_mfma_clock(clocks: torch.Tensor, iters: int, tflops: Optional[float] = None) -> dict:
+    """From the counters ``probe_mfma`` recorded: the matrix pipes' busy
+    fraction over each wavefront's loop in shader-clock cycles (two
+    wavefronts per SIMD, 32 cycles per instruction), and the shader clock
+    against the real-time counter taken at 100 MHz. With ``tflops`` (the
+    probe's measured rate) also the clock that rate implies at that busy
+    fraction, 256 CUs x 4096 FLOP per cycle; the real-time counter's rate
+    has disagreed with it by up to 15% on some boxes, so the implied clock is
+    the one to use."""
     c = clocks.view(-1, 4).cpu().double()
     dt, dr = c[:, 1] - c[:, 0], c[:, 3] - c[:, 2]
     ok = dr > 0
     ghz = (dt[ok] / dr[ok] * 0.1).median().item()
     busy = (2 * 8 * iters * 32 / dt[ok]).median().item()
-    return {"clock_ghz_median": round(ghz, 3), "matrix_busy_median": round(busy, 4)}
+    r = {"matrix_busy_median": round(busy, 4), "clock_ghz_realtime_median": round(ghz, 3)}
+    if tflops is not None:
+        r["clock_ghz_implied"] = round(tflops / (256 * 4096 * busy) * 1e3, 3)
+    return r
 
 
 def probe_read_blocks_waves(num_seqs: int, num_kv_heads: int, max_seq_len: int) -> int:
