@@ -170,7 +170,8 @@ def read_ceiling(args, K, b, kv, bt, sl, nbytes, split_ms):
 
 def mfma_ceiling(args, K, prefill_tflops):
     """The matrix-unit rate this chip sustains in the prefill kernel's launch
-    shape with random bf16 operands (the matrix probe, 8 workgroups per CU)."""
+    shape with random bf16 operands (the matrix probe: 2048 workgroups of
+    eight wavefronts, one resident per CU at a time)."""
     wg, iters = 256 * 8, 2000
     out = torch.empty(wg * K.lib().kvattn_probe_mfma_threads(), dtype=torch.float32,
                       device="cuda")
